@@ -1,0 +1,211 @@
+#!/usr/bin/env python3
+"""Benchmark of one mixed RT/BE paged-attention step on one MI355X.
+
+A step is the whole hot path over one synthetic batch whose KV lives in one
+shared bidirectional pool: bros_kv_write of the step's new tokens, then
+bros_attn_prefill_chunk for the RT prefill chunks, then bros_attn_decode for
+the BE decode rows. Default workload: llama3-8b-mixed-step (4 RT chunks of 512
+new tokens on c0 ~ U{0..2048} cached tokens, 128 BE decode rows with ctx ~
+U{512..8192}, 32 q / 8 KV heads, head_dim 128, bf16, 40000-block pool).
+
+Timing: inputs resident in HBM; W untimed warm-up steps, then exactly K steps
+between two synchronizations, with HIP events around each of the three calls
+on the stream they run on. Prints ONE JSON line:
+  value     = algorithmic bytes of a step / step time (GB/s, whole job)
+  roofline  = the dominant call (decode): algorithmic bytes per launch / its
+              average event-timed duration, against 8 TB/s HBM
+  cpu_baseline = the CPU oracle on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
+METRIC = "µs per mixed RT/BE attention step + achieved KV GB/s (% of HBM peak)"
+
+
+def algorithmic_work(batch):
+    """Bytes and flops the method must move / do for one step, per call."""
+    e = batch.elem_bytes
+    hkv, hq, d = batch.num_kv_heads, batch.num_q_heads, batch.head_dim
+    P = batch.num_prefill
+    kv_tok = 2 * hkv * d * e                         # K + V bytes of one token
+    ctx = batch.ctx_lens.astype(np.int64)
+    dec_rows = batch.num_seqs - P
+    dec_kv = int(ctx[P:].sum()) * kv_tok
+    dec_qo = 2 * dec_rows * hq * d * e
+    dec_tables = int(((ctx[P:] + 15) // 16).sum()) * 4 + dec_rows * (4 + 1)
+    pre_kv = int(ctx[:P].sum()) * kv_tok             # each chunk reads its context once
+    tq = int(batch.cu_q[-1])
+    pre_qo = 2 * tq * hq * d * e
+    n = np.diff(batch.cu_q).astype(np.int64)
+    c0 = ctx[:P] - n
+    # causal flops: QK^T and PV, 2 flops per MAC each
+    pre_flops = int(sum(4 * hq * d * int(np.sum(c0[i] + np.arange(1, n[i] + 1))) for i in range(P)))
+    tn = int(batch.cu_new[-1])
+    write_bytes = 2 * tn * kv_tok                    # read the new rows, write them into the pool
+    return {
+        "kv_write": {"bytes": write_bytes},
+        "prefill": {"bytes": pre_kv + pre_qo, "flops": pre_flops},
+        "decode": {"bytes": dec_kv + dec_qo + dec_tables, "kv_bytes": dec_kv},
+        "step_bytes": write_bytes + pre_kv + pre_qo + dec_kv + dec_qo + dec_tables,
+    }
+
+
+def cpu_baseline(batch, budget_s: float):
+    """Time the oracle (as it stands) on a bounded sample of this workload:
+    decode rows in batch order until the budget is used, plus the whole first
+    prefill chunk. Returns GB/s of algorithmic bytes processed."""
+    import oracle
+    t0 = time.perf_counter()
+    P = batch.num_prefill
+    e = batch.elem_bytes
+    kv_tok = 2 * batch.num_kv_heads * batch.head_dim * e
+    done_bytes = 0
+    desc = []
+    if P:
+        oracle.prefill_chunk(batch.q_prefill, batch.cu_q, batch.k_pool, batch.v_pool, batch.block_tables[:P],
+                             batch.dir[:P], batch.ctx_lens[:P], batch.dtype, seqs=[0])
+        done_bytes += int(batch.ctx_lens[0]) * kv_tok
+        desc.append(f"prefill chunk 0 ({int(batch.cu_q[1])} rows, ctx {int(batch.ctx_lens[0])})")
+    rows = 0
+    for s in range(batch.num_seqs - P):
+        if time.perf_counter() - t0 > budget_s:
+            break
+        oracle.decode(batch.q_decode, batch.k_pool, batch.v_pool, batch.block_tables[P:], batch.dir[P:],
+                      batch.ctx_lens[P:], batch.dtype, seqs=[s])
+        done_bytes += int(batch.ctx_lens[P + s]) * kv_tok
+        rows += 1
+    dt = time.perf_counter() - t0
+    desc.append(f"{rows} of {batch.num_seqs - P} decode rows")
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([1] + [int(p.get("num_threads", 1)) for p in threadpool_info()])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    return {"value": done_bytes / dt / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": "; ".join(desc) + f"; {dt:.1f} s fp64 NumPy", "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama3-8b-mixed-step")
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--overlap", action="store_true", help="run the prefill on a side stream beside the decode")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--check", action="store_true", help="check the benchmarked step against the oracle first")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the step shards by KV head or by sequence with no exchange, but only the one-GPU path is built)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    from paper_2504_09590_amd import bros, workload
+    from paper_2504_09590_amd.step import MixedStep
+
+    batch = workload.generate(args.workload, seed=args.seed)
+    bros.bros_check_batch(batch.block_tables, batch.dir, batch.cls, batch.ctx_lens, batch.num_blocks)
+    dev = bros.to_device(batch)
+    step = MixedStep(batch, dev, overlap=args.overlap)
+    work = algorithmic_work(batch)
+    stream = torch.cuda.current_stream()
+
+    if args.check:
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from tests.gpu_helpers import compare, oracle_step
+        k1, v1, pre_ref, dec_ref = oracle_step(batch)
+        pre, dec = step.run()
+        torch.cuda.synchronize()
+        if batch.num_prefill:
+            compare(bros.to_host_bits(pre), pre_ref, batch.dtype, "prefill")
+        compare(bros.to_host_bits(dec), dec_ref, batch.dtype, "decode")
+        print("check: step matches the oracle", file=sys.stderr)
+
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+          for k in ("kv_write", "prefill", "decode")}
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(K):
+        if args.overlap:
+            step.run()
+        else:
+            a, b = ev["kv_write"][i]
+            a.record(stream); step.kv_write(stream); b.record(stream)
+            a, b = ev["prefill"][i]
+            a.record(stream); step.prefill(stream); b.record(stream)
+            a, b = ev["decode"][i]
+            a.record(stream); step.decode(stream); b.record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    ms = start.elapsed_time(end) / K
+
+    per_call = {}
+    if not args.overlap:
+        for k, pairs in ev.items():
+            per_call[k] = float(np.mean([a.elapsed_time(b) for a, b in pairs]))
+
+    dec_ms = per_call.get("decode")
+    roof = None
+    if dec_ms:
+        achieved = work["decode"]["bytes"] / (dec_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "bros_attn_decode (decode_split_kernel + decode_merge_kernel)",
+                "bytes_per_launch": work["decode"]["bytes"], "avg_launch_us": round(dec_ms * 1e3, 2)}
+
+    value = work["step_bytes"] / (ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "us_per_step": round(ms * 1e3, 2),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": batch.dtype,
+        "data": "synthetic", "hbm_frac_step": round(value / HBM_PEAK_GBS, 4),
+        "config": {"workload": batch.name, "seed": batch.seed, "num_seqs": batch.num_seqs,
+                   "prefill_chunks": batch.num_prefill, "decode_rows": batch.num_seqs - batch.num_prefill,
+                   "q_heads": batch.num_q_heads, "kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim,
+                   "block_size": 16, "pool_blocks": batch.num_blocks, "sum_ctx": int(batch.ctx_lens.sum()),
+                   "overlap": bool(args.overlap)},
+        "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
+        "step_bytes": work["step_bytes"],
+        "roofline": roof,
+        "wall_ms_timed_region": round(wall_ms, 3),
+    }
+    if per_call.get("prefill"):
+        tf = work["prefill"]["flops"] / (per_call["prefill"] * 1e-3) / 1e12
+        line["prefill_mfma"] = {"achieved_tflops": round(tf, 1), "peak_tflops": BF16_MFMA_PEAK_TFLOPS,
+                                "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "flops": work["prefill"]["flops"]}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

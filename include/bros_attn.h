@@ -1,0 +1,212 @@
+/*
+ * bros_attn.h -- C ABI of the MI355X (gfx950) bidirectional paged-attention step.
+ *
+ * One serving iteration over a mixed batch of real-time (RT) and best-effort
+ * (BE) requests whose KV cache lives in ONE shared pool of 16-slot blocks with
+ * the bidirectional layout of "Efficient LLM Serving on Hybrid Real-time and
+ * Best-effort Requests" (arXiv 2504.09590):
+ *
+ *   - Sec. 5.1 (Block Structure): a block can hold one RT and one BE request;
+ *     the RT request's tokens fill its slots from the left end, the BE
+ *     request's from the right end; a request may span several blocks.
+ *   - Sec. 5.2 (Block Management, lazy checkpointing): while free slots remain
+ *     each request treats a shared block as its own, so entry i of a request's
+ *     block table holds its logical positions [16 i, 16 i + 16).
+ *   - Sec. 6 (Implementation): the attention kernel receives the block tables
+ *     plus a direction flag telling whether a block's slots are walked from the
+ *     left or from the right; prefill rows of the batch are concatenated along
+ *     the token axis with a length table, decode rows follow.
+ *
+ * Slot of logical position p of a sequence with direction d:
+ *     block = block_tables[s][p / 16],  slot = (d == +1) ? p % 16 : 15 - p % 16.
+ *
+ * COMMON CONVENTIONS
+ *   Pointers named *_pool, q, out, k_new, v_new, block_tables, dir, cls,
+ *   ctx_lens, pos0, cu_new, cu_q and workspace are HIP DEVICE pointers, owned
+ *   by the caller, row-major and contiguous. The library allocates nothing per
+ *   call, keeps no state between calls, never synchronizes, and enqueues its
+ *   kernels on `stream` (a hipStream_t; NULL = the null stream). Calls on
+ *   different streams touching disjoint outputs may run concurrently.
+ *
+ *   Pool layout:  k_pool, v_pool  [num_blocks][num_kv_heads][16][head_dim]
+ *                 (one (block, KV head) tile = 16 x head_dim contiguous values).
+ *   dtype:        BROS_F32 or BROS_BF16; q, pools, k_new/v_new and out share it.
+ *                 Arithmetic accumulates in fp32; bf16 outputs are rounded to
+ *                 nearest-even.
+ *   dir:          int8 [num_seqs], +1 (left-to-right) or -1 (right-to-left).
+ *                 May be NULL: then the direction is derived from cls
+ *                 (RT -> +1, BE -> -1), which is the layout of Sec. 5.1.
+ *   cls:          uint8 [num_seqs], BROS_RT or BROS_BE. Only consulted when
+ *                 dir is NULL; it has no other numerical effect. May be NULL
+ *                 when dir is given.
+ *   block_tables: int32 [num_seqs][max_blocks_per_seq]; entries at index
+ *                 >= ceil(ctx / 16) are never read.
+ *   ctx_lens:     int32 [num_seqs], tokens in the cache AFTER this step's
+ *                 writes (a decode sequence's count includes its new token).
+ *   Supported shapes: block_size == 16, head_dim == 128, num_q_heads a
+ *   multiple of num_kv_heads with group size 1, 2, 4 or 8.
+ *
+ *   Block-table contents are NOT validated in the hot path (that would need a
+ *   device-to-host copy). The kernels never touch memory outside the buffers
+ *   whatever the tables hold: an entry outside [0, num_blocks) or a context
+ *   longer than max_blocks_per_seq * 16 makes the affected tokens contribute
+ *   nothing (attention) or not be written (kv_write). bros_check_batch() runs
+ *   the full consistency check on host copies.
+ *
+ * ERRORS
+ *   Every entry point returns BROS_OK (0) or a negative status; nothing is
+ *   launched when the status is negative, except BROS_E_HIP which reports a
+ *   launch failure. bros_last_error() returns a thread-local message describing
+ *   the most recent failure on the calling thread. No exception crosses the ABI.
+ */
+#ifndef BROS_ATTN_H
+#define BROS_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum bros_dtype { BROS_F32 = 0, BROS_BF16 = 1 };
+enum bros_class { BROS_RT = 0, BROS_BE = 1 };
+enum bros_status {
+  BROS_OK = 0,
+  BROS_E_NULL = -1,        /* a required pointer is NULL                               */
+  BROS_E_SHAPE = -2,       /* inconsistent sizes (Hq % Hkv, negative counts, ...)        */
+  BROS_E_DTYPE = -3,       /* dtype is neither BROS_F32 nor BROS_BF16                   */
+  BROS_E_UNSUPPORTED = -4, /* block_size != 16, head_dim != 128, group not in {1,2,4,8} */
+  BROS_E_WORKSPACE = -5,   /* workspace missing or smaller than the size query's answer */
+  BROS_E_HIP = -6,         /* a HIP launch failed; message carries hipGetErrorString    */
+  BROS_E_TABLE = -7        /* bros_check_batch found an inconsistent batch               */
+};
+enum bros_workspace_kind { BROS_WS_DECODE = 0, BROS_WS_PREFILL = 1 };
+
+/* Static string naming a status code. */
+const char* bros_status_str(int status);
+/* Message of the last failure on the calling thread ("" if none). */
+const char* bros_last_error(void);
+/* ABI version of this library (increments on any signature change). */
+int bros_abi_version(void);
+
+/*
+ * bros_kv_write -- store this step's new tokens in their bidirectional slots.
+ *
+ * Defines: Sec. 5.1 (RT fills a block from the left, BE from the right) with
+ * the exclusive view of Sec. 5.2. For every sequence s and every new token t
+ * in [cu_new[s], cu_new[s+1]), at logical position p = pos0[s] + t - cu_new[s]:
+ *     k_pool[block][h][slot][:] = k_new[t][h][:]   for every KV head h,
+ *     v_pool[block][h][slot][:] = v_new[t][h][:],
+ * with (block, slot) from the mapping above. Pure data movement: the pool
+ * bytes at every written slot equal the source bytes; no other byte changes.
+ * Two sequences sharing a block write disjoint slots in the same launch.
+ *
+ *   k_new, v_new : [num_new_tokens][num_kv_heads][head_dim]
+ *   pos0         : int32 [num_seqs], logical position of each sequence's first new token
+ *   cu_new       : int32 [num_seqs + 1], prefix offsets of new tokens; cu_new[0] = 0,
+ *                  cu_new[num_seqs] = num_new_tokens
+ * num_new_tokens == 0 is a no-op. A token whose block-table entry is out of
+ * range (see COMMON CONVENTIONS) is skipped.
+ */
+int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
+                  void* k_pool, void* v_pool, int32_t num_blocks,
+                  const int32_t* block_tables, int32_t max_blocks_per_seq,
+                  const int8_t* dir, const uint8_t* cls,
+                  const int32_t* pos0, const int32_t* cu_new,
+                  int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
+                  int32_t block_size, int32_t dtype, void* stream);
+
+/*
+ * bros_attn_decode -- one query row per sequence over its whole paged context.
+ *
+ * Defines: the decode attention of Sec. 2.1 (the new token attends to the
+ * cached keys/values of all earlier tokens and itself) run over the
+ * direction-aware paged layout of Sec. 5.1 / Sec. 6. For sequence s and query
+ * head h, with g = h / (num_q_heads / num_kv_heads) and the keys/values of
+ * positions p < ctx_lens[s] gathered through the block table:
+ *     out[s][h][:] = sum_p softmax_p(scale * q[s][h] . K[p][g]) * V[p][g][:].
+ * A sequence with ctx_lens[s] <= 0 gets a zero output row.
+ *
+ *   q, out       : [num_seqs][num_q_heads][head_dim]
+ *   max_ctx      : host-side upper bound of every ctx_lens[s]; sizes the grid
+ *                  and the workspace without a device-to-host copy. Contexts
+ *                  above it are truncated to max_ctx.
+ *   scale        : softmax scale; <= 0 selects 1 / sqrt(head_dim)
+ *   workspace    : device scratch of at least
+ *                  bros_attn_workspace_size(BROS_WS_DECODE, dtype, num_seqs,
+ *                  num_q_heads, head_dim, max_ctx) bytes (may be NULL when that
+ *                  size is 0). Holds split-K partial results; overwritten.
+ */
+int bros_attn_decode(void* out, const void* q,
+                     const void* k_pool, const void* v_pool, int32_t num_blocks,
+                     const int32_t* block_tables, int32_t max_blocks_per_seq,
+                     const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                     int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
+                     int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                     float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+/*
+ * bros_attn_prefill_chunk -- causal attention of RT prefill chunks over the pool.
+ *
+ * Defines: the prefill half of the mixed batch of Sec. 6 (prefill rows
+ * concatenated along the token axis, their shapes in a length table), with
+ * chunked prefill on top of already-cached context (Sec. 2.2 / Sec. 8). Rows
+ * of sequence s are q[cu_q[s] .. cu_q[s+1]); with n = cu_q[s+1] - cu_q[s] and
+ * c0 = ctx_lens[s] - n (the chunk's K/V already stored by bros_kv_write), row j
+ * sits at position c0 + j and attends to positions 0 .. c0 + j (diagonal
+ * inclusive), with the same head grouping and gather as bros_attn_decode.
+ * Sequences with n == 0 are skipped.
+ *
+ *   q, out       : [num_q_tokens][num_q_heads][head_dim]
+ *   cu_q         : int32 [num_seqs + 1], prefix offsets; cu_q[num_seqs] = num_q_tokens
+ *   max_q_len    : host-side upper bound of every n (sizes the grid)
+ *   max_ctx      : host-side upper bound of every ctx_lens[s]
+ *   workspace    : at least bros_attn_workspace_size(BROS_WS_PREFILL, dtype,
+ *                  num_q_tokens, num_q_heads, head_dim, max_ctx) bytes.
+ * bf16 runs the QK^T and PV products on the matrix cores (P is rounded to bf16
+ * before PV); fp32 runs a vector-ALU path.
+ */
+int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
+                            int32_t num_q_tokens, int32_t max_q_len,
+                            const void* k_pool, const void* v_pool, int32_t num_blocks,
+                            const int32_t* block_tables, int32_t max_blocks_per_seq,
+                            const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                            int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
+                            int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                            float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/*
+ * Bytes of device workspace the call `kind` needs for `num_rows` query rows
+ * (num_seqs for decode, num_q_tokens for prefill). Pure host arithmetic.
+ * Returns 0 for unsupported arguments.
+ */
+size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
+                                int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);
+
+/*
+ * bros_check_batch -- full host-side consistency check of a batch's metadata.
+ *
+ * Defines: the invariant behind Sec. 5.2 (two requests sharing a block never
+ * own the same slot; a peer's token that would be overwritten is checkpointed
+ * first, so a consistent batch maps distinct (sequence, position) pairs to
+ * distinct (block, slot) pairs). All pointers are HOST pointers. Checks, in
+ * order: counts and pointers, dir values in {+1, -1} (or cls in {RT, BE} when
+ * dir is NULL), 0 <= ctx_lens[s] <= max_blocks_per_seq * 16, every referenced
+ * table entry in [0, num_blocks), and -- when check_slot_disjointness != 0 --
+ * that no (block, slot) is owned twice. Returns BROS_OK or BROS_E_TABLE (or
+ * BROS_E_NULL / BROS_E_SHAPE / BROS_E_UNSUPPORTED) with a message naming the
+ * first offending sequence and position.
+ */
+int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_per_seq,
+                     const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                     int32_t num_seqs, int32_t num_blocks, int32_t block_size,
+                     int32_t check_slot_disjointness);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BROS_ATTN_H */

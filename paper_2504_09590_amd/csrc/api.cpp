@@ -1,0 +1,219 @@
+// C ABI of the bidirectional paged-attention step: O(1) argument checks,
+// launch planning, kernel launches, status strings. No per-call allocation,
+// no synchronization, no state kept between calls.
+#include "bros_attn.h"
+#include "bros_error.h"
+#include "bros_kernels.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+namespace {
+
+using bros::fail;
+using bros::ok;
+
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+// Checks shared by the three entry points; sets *group on success.
+int check_shapes(const char* fn, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                 int32_t block_size, int32_t dtype, int* group) {
+  if (dtype != BROS_F32 && dtype != BROS_BF16) return fail(BROS_E_DTYPE, "%s: dtype %d is neither BROS_F32 nor BROS_BF16", fn, dtype);
+  if (block_size != 16) return fail(BROS_E_UNSUPPORTED, "%s: block_size %d unsupported (16 only)", fn, block_size);
+  if (head_dim != 128) return fail(BROS_E_UNSUPPORTED, "%s: head_dim %d unsupported (128 only)", fn, head_dim);
+  if (num_kv_heads <= 0 || num_q_heads <= 0) return fail(BROS_E_SHAPE, "%s: head counts must be positive (Hq=%d Hkv=%d)", fn, num_q_heads, num_kv_heads);
+  if (num_q_heads % num_kv_heads != 0) return fail(BROS_E_SHAPE, "%s: num_q_heads %d is not a multiple of num_kv_heads %d", fn, num_q_heads, num_kv_heads);
+  const int g = num_q_heads / num_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8) return fail(BROS_E_UNSUPPORTED, "%s: group size %d unsupported (1, 2, 4 or 8)", fn, g);
+  *group = g;
+  return BROS_OK;
+}
+
+int check_meta(const char* fn, const void* block_tables, int32_t max_blocks_per_seq, const int8_t* dir,
+               const uint8_t* cls, int32_t num_blocks) {
+  if (block_tables == nullptr) return fail(BROS_E_NULL, "%s: block_tables is NULL", fn);
+  if (dir == nullptr && cls == nullptr) return fail(BROS_E_NULL, "%s: dir and cls are both NULL", fn);
+  if (max_blocks_per_seq <= 0) return fail(BROS_E_SHAPE, "%s: max_blocks_per_seq %d must be positive", fn, max_blocks_per_seq);
+  if (num_blocks <= 0) return fail(BROS_E_SHAPE, "%s: num_blocks %d must be positive", fn, num_blocks);
+  if (!aligned(block_tables, 4)) return fail(BROS_E_SHAPE, "%s: block_tables is not 4-byte aligned", fn);
+  return BROS_OK;
+}
+
+int launch_status(const char* fn, hipError_t e) {
+  if (e != hipSuccess) return fail(BROS_E_HIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+float resolve_scale(float scale, int head_dim) {
+  const float s = scale > 0.0f ? scale : 1.0f / std::sqrt((float)head_dim);
+  return s * 1.4426950408889634f;   // log2(e): the kernels use base-2 exponentials
+}
+
+}  // namespace
+
+extern "C" {
+
+int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
+                  void* k_pool, void* v_pool, int32_t num_blocks,
+                  const int32_t* block_tables, int32_t max_blocks_per_seq,
+                  const int8_t* dir, const uint8_t* cls,
+                  const int32_t* pos0, const int32_t* cu_new,
+                  int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
+                  int32_t block_size, int32_t dtype, void* stream) {
+  const char* fn = "bros_kv_write";
+  int group = 0;
+  int st = check_shapes(fn, num_kv_heads, num_kv_heads, head_dim, block_size, dtype, &group);
+  if (st) return st;
+  if (num_new_tokens < 0 || num_seqs < 0) return fail(BROS_E_SHAPE, "%s: negative count (tokens=%d seqs=%d)", fn, num_new_tokens, num_seqs);
+  if (num_new_tokens == 0) return ok();
+  if (num_seqs == 0) return fail(BROS_E_SHAPE, "%s: %d new tokens but no sequences", fn, num_new_tokens);
+  if (!k_new || !v_new || !k_pool || !v_pool || !pos0 || !cu_new) return fail(BROS_E_NULL, "%s: a tensor or offset pointer is NULL", fn);
+  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, num_blocks);
+  if (st) return st;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16))
+    return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
+  bros::KvWriteArgs a{k_new, v_new, k_pool, v_pool, block_tables, dir, cls, pos0, cu_new,
+                      num_new_tokens, num_seqs, num_blocks, max_blocks_per_seq, num_kv_heads};
+  return launch_status(fn, bros::launch_kv_write(a, dtype == BROS_BF16, static_cast<hipStream_t>(stream)));
+}
+
+size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
+                                int32_t num_q_heads, int32_t head_dim, int32_t max_ctx) {
+  if (num_rows <= 0 || num_q_heads <= 0 || head_dim != 128 || max_ctx < 0) return 0;
+  if (dtype != BROS_F32 && dtype != BROS_BF16) return 0;
+  if (kind == BROS_WS_DECODE) return bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx);
+  if (kind == BROS_WS_PREFILL) return dtype == BROS_BF16 ? 0 : bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx);
+  return 0;
+}
+
+int bros_attn_decode(void* out, const void* q,
+                     const void* k_pool, const void* v_pool, int32_t num_blocks,
+                     const int32_t* block_tables, int32_t max_blocks_per_seq,
+                     const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                     int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
+                     int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                     float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  const char* fn = "bros_attn_decode";
+  int group = 0;
+  int st = check_shapes(fn, num_q_heads, num_kv_heads, head_dim, block_size, dtype, &group);
+  if (st) return st;
+  if (num_seqs < 0 || max_ctx < 0) return fail(BROS_E_SHAPE, "%s: negative count (seqs=%d max_ctx=%d)", fn, num_seqs, max_ctx);
+  if (num_seqs == 0) return ok();
+  if (!out || !q || !k_pool || !v_pool || !ctx_lens) return fail(BROS_E_NULL, "%s: a tensor or length pointer is NULL", fn);
+  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, num_blocks);
+  if (st) return st;
+  if (!aligned(out, 16) || !aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16))
+    return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
+  const size_t need = bros::decode_workspace_bytes(num_seqs, num_q_heads, max_ctx);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 16)))
+    return fail(BROS_E_WORKSPACE, "%s: workspace of %zu bytes (16-byte aligned) required, got %zu at %p", fn, need, workspace_bytes, workspace);
+  const bros::DecodePlan plan = bros::plan_decode(num_seqs, max_ctx);
+  bros::DecodeArgs a{};
+  a.out = out;
+  a.q = q;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.block_tables = block_tables;
+  a.dir = dir;
+  a.cls = cls;
+  a.ctx_lens = ctx_lens;
+  a.cu_q = nullptr;
+  a.ws_acc = static_cast<float*>(workspace);
+  a.ws_ml = need > 0 ? static_cast<float*>(workspace) + (size_t)num_seqs * num_q_heads * plan.n_split_max * head_dim : nullptr;
+  a.num_rows = num_seqs;
+  a.num_seqs = num_seqs;
+  a.num_blocks = num_blocks;
+  a.max_blocks_per_seq = max_blocks_per_seq;
+  a.max_ctx = max_ctx;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.split_blocks = plan.split_blocks;
+  a.n_split_max = plan.n_split_max;
+  a.scale_log2 = resolve_scale(scale, head_dim);
+  return launch_status(fn, bros::launch_decode(a, group, dtype == BROS_BF16, static_cast<hipStream_t>(stream)));
+}
+
+int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
+                            int32_t num_q_tokens, int32_t max_q_len,
+                            const void* k_pool, const void* v_pool, int32_t num_blocks,
+                            const int32_t* block_tables, int32_t max_blocks_per_seq,
+                            const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                            int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
+                            int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                            float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  const char* fn = "bros_attn_prefill_chunk";
+  int group = 0;
+  int st = check_shapes(fn, num_q_heads, num_kv_heads, head_dim, block_size, dtype, &group);
+  if (st) return st;
+  if (num_seqs < 0 || num_q_tokens < 0 || max_q_len < 0 || max_ctx < 0)
+    return fail(BROS_E_SHAPE, "%s: negative count (seqs=%d tokens=%d max_q_len=%d max_ctx=%d)", fn, num_seqs, num_q_tokens, max_q_len, max_ctx);
+  if (num_seqs == 0 || num_q_tokens == 0) return ok();
+  if (max_q_len == 0) return fail(BROS_E_SHAPE, "%s: max_q_len is 0 with %d query rows", fn, num_q_tokens);
+  if (!out || !q || !cu_q || !k_pool || !v_pool || !ctx_lens) return fail(BROS_E_NULL, "%s: a tensor or length pointer is NULL", fn);
+  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, num_blocks);
+  if (st) return st;
+  if (!aligned(out, 16) || !aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16))
+    return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const float scale_log2 = resolve_scale(scale, head_dim);
+
+  if (dtype == BROS_BF16) {
+    bros::PrefillArgs a{};
+    a.out = out;
+    a.q = q;
+    a.cu_q = cu_q;
+    a.k_pool = k_pool;
+    a.v_pool = v_pool;
+    a.block_tables = block_tables;
+    a.dir = dir;
+    a.cls = cls;
+    a.ctx_lens = ctx_lens;
+    a.num_q_tokens = num_q_tokens;
+    a.num_seqs = num_seqs;
+    a.num_blocks = num_blocks;
+    a.max_blocks_per_seq = max_blocks_per_seq;
+    a.max_ctx = max_ctx;
+    a.num_q_heads = num_q_heads;
+    a.num_kv_heads = num_kv_heads;
+    const int qt = bros::prefill_positions_per_tile(group);
+    a.tiles_per_seq = (max_q_len + qt - 1) / qt;
+    a.scale_log2 = scale_log2;
+    const long long total = (long long)num_seqs * num_kv_heads * a.tiles_per_seq;
+    if (total > 0x7fffffffLL) return fail(BROS_E_SHAPE, "%s: grid of %lld workgroups too large", fn, total);
+    return launch_status(fn, bros::launch_prefill_mfma(a, group, (int)total, s));
+  }
+
+  // fp32: every prefill row is a decode row with its own causal context.
+  const size_t need = bros::decode_workspace_bytes(num_q_tokens, num_q_heads, max_ctx);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 16)))
+    return fail(BROS_E_WORKSPACE, "%s: workspace of %zu bytes (16-byte aligned) required, got %zu at %p", fn, need, workspace_bytes, workspace);
+  const bros::DecodePlan plan = bros::plan_decode(num_q_tokens, max_ctx);
+  bros::DecodeArgs a{};
+  a.out = out;
+  a.q = q;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.block_tables = block_tables;
+  a.dir = dir;
+  a.cls = cls;
+  a.ctx_lens = ctx_lens;
+  a.cu_q = cu_q;
+  a.ws_acc = static_cast<float*>(workspace);
+  a.ws_ml = need > 0 ? static_cast<float*>(workspace) + (size_t)num_q_tokens * num_q_heads * plan.n_split_max * head_dim : nullptr;
+  a.num_rows = num_q_tokens;
+  a.num_seqs = num_seqs;
+  a.num_blocks = num_blocks;
+  a.max_blocks_per_seq = max_blocks_per_seq;
+  a.max_ctx = max_ctx;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.split_blocks = plan.split_blocks;
+  a.n_split_max = plan.n_split_max;
+  a.scale_log2 = scale_log2;
+  return launch_status(fn, bros::launch_decode(a, group, false, s));
+}
+
+}  // extern "C"

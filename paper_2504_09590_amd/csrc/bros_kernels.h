@@ -1,0 +1,89 @@
+// Internal launch interface between the C ABI layer (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bros {
+
+struct KvWriteArgs {
+  const void* k_new;
+  const void* v_new;
+  void* k_pool;
+  void* v_pool;
+  const int32_t* block_tables;
+  const int8_t* dir;
+  const uint8_t* cls;
+  const int32_t* pos0;
+  const int32_t* cu_new;
+  int32_t num_new_tokens;
+  int32_t num_seqs;
+  int32_t num_blocks;
+  int32_t max_blocks_per_seq;
+  int32_t num_kv_heads;
+};
+
+// Split-K decode over "query rows". In decode mode (cu_q == nullptr) row r is
+// sequence r with context ctx_lens[r]. In row mode (cu_q != nullptr) row r is a
+// prefill row of the sequence s with cu_q[s] <= r < cu_q[s+1] and sees the
+// first ctx_lens[s] - (cu_q[s+1] - r) + 1 positions (causal, diagonal inclusive).
+struct DecodeArgs {
+  void* out;
+  const void* q;
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* block_tables;
+  const int8_t* dir;
+  const uint8_t* cls;
+  const int32_t* ctx_lens;
+  const int32_t* cu_q;
+  float* ws_acc;          // [rows][Hq][n_split_max][D] unnormalised partial outputs
+  float* ws_ml;           // [rows][Hq][n_split_max][2] (running max in log2 units, sum)
+  int32_t num_rows;
+  int32_t num_seqs;
+  int32_t num_blocks;
+  int32_t max_blocks_per_seq;
+  int32_t max_ctx;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t split_blocks;   // blocks per split, multiple of 4, <= 64
+  int32_t n_split_max;
+  float scale_log2;       // softmax scale * log2(e)
+};
+
+struct PrefillArgs {
+  void* out;
+  const void* q;
+  const int32_t* cu_q;
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* block_tables;
+  const int8_t* dir;
+  const uint8_t* cls;
+  const int32_t* ctx_lens;
+  int32_t num_q_tokens;
+  int32_t num_seqs;
+  int32_t num_blocks;
+  int32_t max_blocks_per_seq;
+  int32_t max_ctx;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t tiles_per_seq;  // ceil(max_q_len / positions per tile)
+  float scale_log2;
+};
+
+// Decode planning shared by the launcher and the workspace query.
+struct DecodePlan {
+  int32_t split_blocks;
+  int32_t n_split_max;
+};
+DecodePlan plan_decode(int32_t num_rows, int32_t max_ctx);
+size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max_ctx);
+
+hipError_t launch_kv_write(const KvWriteArgs& a, bool bf16, hipStream_t stream);
+hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream);
+hipError_t launch_prefill_mfma(const PrefillArgs& a, int group, int num_tiles_total, hipStream_t stream);
+int prefill_positions_per_tile(int group);
+
+}  // namespace bros

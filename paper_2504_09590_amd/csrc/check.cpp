@@ -1,0 +1,63 @@
+// bros_check_batch: host-side consistency check of one batch's metadata.
+//
+// Two sequences may share a block (an RT tail from the left end, a BE tail
+// from the right end, Sec. 5.1), but a consistent batch never maps two valid
+// (sequence, position) pairs to one (block, slot): the paper checkpoints a
+// peer's token before it is overwritten (Sec. 5.2). This checker is pure C++
+// and runs on host copies; the kernels rely on it rather than re-validating
+// tables on the device.
+#include "bros_attn.h"
+#include "bros_error.h"
+
+#include <cstdint>
+#include <vector>
+
+using bros::fail;
+
+extern "C" int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                                int32_t num_seqs, int32_t num_blocks, int32_t block_size,
+                                int32_t check_slot_disjointness) {
+  if (block_size != 16) return fail(BROS_E_UNSUPPORTED, "block_size %d unsupported (16 only)", block_size);
+  if (num_seqs < 0 || max_blocks_per_seq <= 0 || num_blocks <= 0)
+    return fail(BROS_E_SHAPE, "bad counts: num_seqs=%d max_blocks_per_seq=%d num_blocks=%d", num_seqs, max_blocks_per_seq, num_blocks);
+  if (num_seqs == 0) return bros::ok();
+  if (!block_tables || !ctx_lens) return fail(BROS_E_NULL, "block_tables or ctx_lens is NULL");
+  if (!dir && !cls) return fail(BROS_E_NULL, "dir and cls are both NULL");
+
+  std::vector<int> d(num_seqs);
+  for (int s = 0; s < num_seqs; ++s) {
+    if (dir) {
+      if (dir[s] != 1 && dir[s] != -1) return fail(BROS_E_TABLE, "sequence %d: direction flag %d is not +1 or -1", s, (int)dir[s]);
+      d[s] = dir[s];
+    } else {
+      if (cls[s] > 1) return fail(BROS_E_TABLE, "sequence %d: class %u is neither RT (0) nor BE (1)", s, (unsigned)cls[s]);
+      d[s] = cls[s] == 1 ? -1 : 1;
+    }
+    if (ctx_lens[s] < 0) return fail(BROS_E_TABLE, "sequence %d: negative context %d", s, ctx_lens[s]);
+    if ((int64_t)ctx_lens[s] > (int64_t)max_blocks_per_seq * 16)
+      return fail(BROS_E_TABLE, "sequence %d: context %d exceeds %d table entries", s, ctx_lens[s], max_blocks_per_seq);
+    const int nblk = (ctx_lens[s] + 15) / 16;
+    for (int b = 0; b < nblk; ++b) {
+      const int32_t id = block_tables[(size_t)s * max_blocks_per_seq + b];
+      if (id < 0 || id >= num_blocks)
+        return fail(BROS_E_TABLE, "sequence %d: table entry %d = %d outside [0, %d)", s, b, id, num_blocks);
+    }
+  }
+  if (!check_slot_disjointness) return bros::ok();
+
+  // One bit per (block, slot); positions < ctx of every sequence must be unique.
+  std::vector<uint16_t> used((size_t)num_blocks, 0);
+  for (int s = 0; s < num_seqs; ++s) {
+    for (int p = 0; p < ctx_lens[s]; ++p) {
+      const int32_t id = block_tables[(size_t)s * max_blocks_per_seq + p / 16];
+      const int off = p % 16;
+      const int slot = d[s] > 0 ? off : 15 - off;
+      const uint16_t bit = (uint16_t)(1u << slot);
+      if (used[id] & bit)
+        return fail(BROS_E_TABLE, "sequence %d position %d: block %d slot %d is already owned by another token", s, p, id, slot);
+      used[id] |= bit;
+    }
+  }
+  return bros::ok();
+}

@@ -1,0 +1,87 @@
+"""One mixed RT/BE attention step: KV write, prefill chunks, decode.
+
+The paper's executor concatenates the prefill requests of a batch, then the
+decode requests, keeps their shapes in a length table and dispatches each half
+to its own attention kernel (Sec. 6). MixedStep is that dispatch over the C ABI:
+sequences [0, P) of the batch are prefill chunks and [P, S) decode rows. Their
+metadata rows are contiguous slices of the batch's tables, so each half gets
+plain pointer offsets into the same device arrays.
+
+Order of one step:  bros_kv_write (all S sequences' new tokens)
+                    -> bros_attn_prefill_chunk (rows of sequences [0, P))
+                    -> bros_attn_decode (sequences [P, S)).
+With overlap=True the prefill runs on a second stream after the write, beside
+the decode, so the matrix-core bound and the HBM bound halves share the chip.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import bros
+
+
+class MixedStep:
+    def __init__(self, batch, dev: bros.DeviceBatch, overlap: bool = False):
+        self.batch = batch
+        self.dev = dev
+        P, S = batch.num_prefill, batch.num_seqs
+        self.P, self.S = P, S
+        self.dtype_code = bros.BROS_F32 if batch.dtype == "f32" else bros.BROS_BF16
+        hq, d = batch.num_q_heads, batch.head_dim
+        self.max_ctx_pre = int(batch.ctx_lens[:P].max()) if P else 0
+        self.max_ctx_dec = int(batch.ctx_lens[P:].max()) if S > P else 0
+        self.max_q_len = int(np.diff(batch.cu_q).max()) if P else 0
+        self.out_prefill = torch.empty_like(dev.q_prefill)
+        self.out_decode = torch.empty_like(dev.q_decode)
+        ws_dec = bros.bros_attn_workspace_size(bros.BROS_WS_DECODE, self.dtype_code, S - P, hq, d, self.max_ctx_dec)
+        ws_pre = bros.bros_attn_workspace_size(bros.BROS_WS_PREFILL, self.dtype_code, int(batch.cu_q[-1]), hq, d,
+                                               self.max_ctx_pre) if P else 0
+        device = dev.k_pool.device
+        self.ws_decode = torch.empty(max(ws_dec, 16), dtype=torch.uint8, device=device) if ws_dec else None
+        self.ws_prefill = torch.empty(max(ws_pre, 16), dtype=torch.uint8, device=device) if ws_pre else None
+        self.overlap = overlap and P > 0 and S > P
+        self.side = torch.cuda.Stream(device=device) if self.overlap else None
+        self._ev_written = torch.cuda.Event() if self.overlap else None
+        self._ev_prefilled = torch.cuda.Event() if self.overlap else None
+
+    # the three calls --------------------------------------------------------
+    def kv_write(self, stream=None):
+        d = self.dev
+        bros.bros_kv_write(d.k_new, d.v_new, d.k_pool, d.v_pool, d.block_tables, d.dir, d.cls,
+                           d.pos0, d.cu_new, stream=stream)
+
+    def prefill(self, stream=None):
+        if self.P == 0:
+            return
+        d, P = self.dev, self.P
+        bros.bros_attn_prefill_chunk(self.out_prefill, d.q_prefill, d.cu_q, self.max_q_len, d.k_pool, d.v_pool,
+                                     d.block_tables[:P], d.dir[:P], d.cls[:P], d.ctx_lens[:P],
+                                     self.max_ctx_pre, workspace=self.ws_prefill, stream=stream)
+
+    def decode(self, stream=None):
+        if self.S == self.P:
+            return
+        d, P = self.dev, self.P
+        bros.bros_attn_decode(self.out_decode, d.q_decode, d.k_pool, d.v_pool, d.block_tables[P:], d.dir[P:],
+                              d.cls[P:], d.ctx_lens[P:], self.max_ctx_dec, workspace=self.ws_decode,
+                              stream=stream)
+
+    def run(self, write: bool = True):
+        """Enqueue one whole step on the current stream (plus the side stream
+        when overlapping); returns (prefill output, decode output)."""
+        main = torch.cuda.current_stream()
+        if write:
+            self.kv_write(main)
+        if self.overlap:
+            self._ev_written.record(main)
+            self.side.wait_event(self._ev_written)
+            self.prefill(self.side)
+            self.decode(main)
+            self._ev_prefilled.record(self.side)
+            main.wait_event(self._ev_prefilled)
+        else:
+            self.prefill(main)
+            self.decode(main)
+        return self.out_prefill, self.out_decode

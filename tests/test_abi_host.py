@@ -1,0 +1,184 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads and exports
+every symbol include/bros_attn.h declares, argument validation rejects bad
+calls before anything is launched, the workspace query is consistent, and the
+batch checker agrees with the oracle's independent slot-ownership count."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_09590_amd import workload as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bros_attn.h")
+
+bros = pytest.importorskip("paper_2504_09590_amd.bros", reason="libbros_attn.so not built")
+
+FAKE = 1 << 20   # a 16-byte aligned non-NULL address; only used on paths rejected before launch
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bros_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_entry_points():
+    names = declared_functions()
+    for fn in ("bros_kv_write", "bros_attn_decode", "bros_attn_prefill_chunk"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(bros.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(bros.EXPORTED) == declared_functions()
+
+
+def test_status_strings_and_version():
+    for code, name in bros.STATUS.items():
+        assert bros.LIB.bros_status_str(code).decode() == name
+    assert bros.LIB.bros_abi_version() == 1
+
+
+# --- argument validation (returns before any HIP call) -----------------------
+
+def _decode(**kw):
+    args = dict(out=FAKE, q=FAKE, k=FAKE, v=FAKE, nb=10, bt=FAKE, maxb=4, dir=FAKE, cls=None,
+                ctx=FAKE, max_ctx=64, S=2, hq=8, hkv=2, d=128, bs=16, scale=0.0, dtype=1,
+                ws=None, wsb=0, stream=None)
+    args.update(kw)
+    return bros.LIB.bros_attn_decode(args["out"], args["q"], args["k"], args["v"], args["nb"], args["bt"],
+                                     args["maxb"], args["dir"], args["cls"], args["ctx"], args["max_ctx"],
+                                     args["S"], args["hq"], args["hkv"], args["d"], args["bs"], args["scale"],
+                                     args["dtype"], args["ws"], args["wsb"], args["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), -3),
+    (dict(d=64), -4),
+    (dict(bs=32), -4),
+    (dict(hq=6, hkv=4), -2),
+    (dict(hq=48, hkv=2), -4),          # group 24
+    (dict(out=None), -1),
+    (dict(bt=None), -1),
+    (dict(dir=None, cls=None), -1),
+    (dict(S=-1), -2),
+    (dict(nb=0), -2),
+    (dict(maxb=0), -2),
+    (dict(out=FAKE + 4), -2),          # misaligned
+    (dict(max_ctx=100000), -5),        # needs a split-K workspace
+])
+def test_decode_rejects(kw, code):
+    assert _decode(**kw) == code
+    assert bros.LIB.bros_last_error().decode() != ""
+
+
+def test_decode_with_no_sequences_is_a_noop():
+    assert _decode(S=0, out=None, q=None) == 0
+
+
+def test_kv_write_rejects():
+    L = bros.LIB
+    args = [FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE, 4, FAKE, None, FAKE, FAKE, 2, 2, 128, 16, 1, None]
+    a = list(args); a[16] = 9
+    assert L.bros_kv_write(*a) == -3
+    a = list(args); a[12] = 0
+    assert L.bros_kv_write(*a) == -2
+    a = list(args); a[10] = None
+    assert L.bros_kv_write(*a) == -1
+    a = list(args); a[2] = 0
+    assert L.bros_kv_write(*a) == 0          # no tokens: no-op
+
+
+def test_prefill_rejects():
+    L = bros.LIB
+    base = [FAKE, FAKE, FAKE, 64, 32, FAKE, FAKE, 10, FAKE, 4, FAKE, None, FAKE, 64, 2, 8, 2, 128, 16,
+            0.0, 1, None, 0, None]
+    a = list(base); a[4] = 0
+    assert L.bros_attn_prefill_chunk(*a) == -2
+    a = list(base); a[2] = None
+    assert L.bros_attn_prefill_chunk(*a) == -1
+    a = list(base); a[20] = 0; a[13] = 100000   # fp32 path needs a workspace
+    assert L.bros_attn_prefill_chunk(*a) == -5
+    a = list(base); a[3] = 0
+    assert L.bros_attn_prefill_chunk(*a) == 0
+
+
+def test_workspace_query():
+    q = bros.bros_attn_workspace_size
+    assert q(0, 1, 4, 8, 128, 64) == 0              # single split: no workspace
+    big = q(0, 1, 64, 32, 128, 8192)
+    assert big > 0 and big % 16 == 0
+    assert q(0, 1, 64, 32, 128, 16384) >= big
+    assert q(1, 1, 2048, 32, 128, 8192) == 0        # bf16 prefill runs on the matrix cores, no scratch
+    assert q(1, 0, 2048, 32, 128, 8192) > 0
+    assert q(0, 1, 4, 8, 64, 64) == 0               # unsupported head_dim
+
+
+# --- the batch checker -------------------------------------------------------
+
+@pytest.mark.parametrize("config", [1, 2, 3, 4, 5])
+def test_checker_accepts_generated_batches(config):
+    b = W.generate(config, with_pool=False)
+    bros.bros_check_batch(b.block_tables, b.dir, b.cls, b.ctx_lens, b.num_blocks)
+    bros.bros_check_batch(b.block_tables, None, b.cls, b.ctx_lens, b.num_blocks)
+
+
+def _tiny():
+    tables = np.array([[2, 0], [3, 0], [1, -1]], dtype=np.int32)
+    return tables, np.array([1, -1, 1], dtype=np.int8), np.array([21, 27, 16], dtype=np.int32)
+
+
+def test_checker_accepts_full_shared_block():
+    t, d, c = _tiny()
+    bros.bros_check_batch(t, d, None, c, 4)
+
+
+@pytest.mark.parametrize("mutate,needle", [
+    (lambda t, d, c: c.__setitem__(1, 28), "already owned"),       # 5 + 12 > 16 slots
+    (lambda t, d, c: t.__setitem__((0, 1), 4), "outside"),
+    (lambda t, d, c: t.__setitem__((0, 0), -3), "outside"),
+    (lambda t, d, c: d.__setitem__(0, 0), "direction"),
+    (lambda t, d, c: c.__setitem__(2, 33), "exceeds"),
+    (lambda t, d, c: c.__setitem__(2, 17), "outside"),             # reaches the -1 pad
+    (lambda t, d, c: c.__setitem__(2, -1), "negative"),
+    (lambda t, d, c: d.__setitem__(1, 1), "already owned"),        # both from the left
+])
+def test_checker_rejects(mutate, needle):
+    t, d, c = _tiny()
+    mutate(t, d, c)
+    with pytest.raises(bros.BrosError) as ei:
+        bros.bros_check_batch(t, d, None, c, 4)
+    assert ei.value.status == -7 and needle in str(ei.value)
+
+
+def test_checker_rejects_unsupported_block_size():
+    t, d, c = _tiny()
+    with pytest.raises(bros.BrosError) as ei:
+        bros.bros_check_batch(t, d, None, c, 4, block_size=8)
+    assert ei.value.status == -4
+
+
+def test_checker_agrees_with_oracle_on_random_batches():
+    rng = np.random.default_rng(3)
+    for trial in range(200):
+        S = int(rng.integers(1, 6))
+        nb = int(rng.integers(1, 8))
+        maxb = int(rng.integers(1, 4))
+        tables = rng.integers(0, nb, size=(S, maxb)).astype(np.int32)
+        dirs = rng.choice([1, -1], size=S).astype(np.int8)
+        ctx = rng.integers(0, maxb * 16 + 1, size=S).astype(np.int32)
+        counts = oracle.slot_owner_counts(tables, dirs, ctx, nb)
+        expect_ok = counts.max(initial=0) <= 1
+        try:
+            bros.bros_check_batch(tables, dirs, None, ctx, nb)
+            got_ok = True
+        except bros.BrosError:
+            got_ok = False
+        assert got_ok == expect_ok, (trial, tables, dirs, ctx)

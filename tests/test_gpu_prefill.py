@@ -1,0 +1,104 @@
+"""bros_attn_prefill_chunk against the oracle.
+
+The pools are written by the oracle's kv_write first (so the chunk's own K/V
+are in place) and then uploaded, so these tests exercise the prefill kernel
+alone. Covers the mixed-step workload's four 512-row chunks, c0 = 0 (pure
+causal), chunk starts and lengths off the 16/64 grid, one-row chunks, RT
+chunks walking from the right, all group sizes, the fp32 path, NaN-poisoned
+unowned slots, and the last row against a decode at the same length."""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_09590_amd import workload as W
+from tests.gpu_helpers import announce, compare, poison_unowned, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def written(batch):
+    """The batch with the oracle's kv_write applied to its pools."""
+    k1, v1 = oracle.kv_write(batch.k_pool, batch.v_pool, batch.k_new, batch.v_new, batch.block_tables,
+                             batch.dir, batch.pos0, batch.cu_new)
+    batch.k_pool, batch.v_pool = k1, v1
+    return batch
+
+
+def run_prefill(batch):
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    dev = bros.to_device(batch)
+    P = batch.num_prefill
+    out = torch.full_like(dev.q_prefill, float("nan"))
+    max_ctx = int(batch.ctx_lens[:P].max())
+    max_q = int(np.diff(batch.cu_q).max())
+    code = bros.BROS_F32 if batch.dtype == "f32" else bros.BROS_BF16
+    wsb = bros.bros_attn_workspace_size(1, code, int(batch.cu_q[-1]), batch.num_q_heads, batch.head_dim, max_ctx)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda") if wsb else None
+    bros.bros_attn_prefill_chunk(out, dev.q_prefill, dev.cu_q, max_q, dev.k_pool, dev.v_pool,
+                                 dev.block_tables[:P], dev.dir[:P], dev.cls[:P], dev.ctx_lens[:P], max_ctx,
+                                 workspace=ws)
+    torch.cuda.synchronize()
+    return bros.to_host_bits(out)
+
+
+def ref_prefill(batch):
+    P = batch.num_prefill
+    return oracle.prefill_chunk(batch.q_prefill, batch.cu_q, batch.k_pool, batch.v_pool, batch.block_tables[:P],
+                                batch.dir[:P], batch.ctx_lens[:P], batch.dtype)
+
+
+def chunk_batch(c0s, ns, classes, group=4, hkv=8, dtype="bf16", seed=0, dirs=None, extra_decode=()):
+    """Prefill sequences first (ctx = c0 + n), then optional decode sequences."""
+    ctx = [c + n for c, n in zip(c0s, ns)] + list(extra_decode)
+    cls = list(classes) + [W.BE] * len(extra_decode)
+    new = list(ns) + [1] * len(extra_decode)
+    if dirs is not None:
+        dirs = list(dirs) + [-1] * len(extra_decode)
+    return W.custom(ctx, cls, hkv * group, hkv, dtype=dtype, seed=seed, num_prefill=len(ns), new_counts=new,
+                    spare_blocks=5, dirs=dirs)
+
+
+def test_mixed_step_workload_prefill_chunks():
+    b = written(W.generate(3))
+    announce(f"prefill llama3-8b-mixed-step chunks c0={(b.ctx_lens[:4] - 512).tolist()}")
+    mx, mean = compare(run_prefill(b), ref_prefill(b), "bf16", "mixed-step prefill")
+    print(f"prefill max {mx:.3g} mean {mean:.3g}")
+
+
+@pytest.mark.parametrize("group", [1, 2, 4, 8])
+def test_ragged_chunks_all_groups(group):
+    b = written(chunk_batch([0, 5, 16, 1000, 63], [37, 1, 100, 300, 65], [W.RT] * 5, group=group, hkv=2,
+                            seed=20 + group, extra_decode=(9, 40)))
+    poison_unowned(b)
+    announce(f"prefill ragged chunks G={group}")
+    compare(run_prefill(b), ref_prefill(b), "bf16", f"ragged G={group}")
+
+
+def test_pure_causal_and_single_row():
+    b = written(chunk_batch([0, 0, 77], [128, 1, 1], [W.RT, W.RT, W.RT], seed=30))
+    poison_unowned(b)
+    announce("prefill c0=0 and one-row chunks")
+    compare(run_prefill(b), ref_prefill(b), "bf16", "causal/single")
+
+
+def test_rt_chunks_walking_from_the_right():
+    b = written(chunk_batch([19, 200], [45, 70], [W.RT, W.RT], dirs=[-1, 1], seed=31))
+    poison_unowned(b)
+    announce("prefill with a right-to-left RT chunk")
+    compare(run_prefill(b), ref_prefill(b), "bf16", "dir -1 chunk")
+
+
+def test_f32_chunks():
+    b = written(chunk_batch([0, 21, 300], [20, 33, 17], [W.RT] * 3, group=4, hkv=2, dtype="f32", seed=32))
+    poison_unowned(b)
+    announce("prefill fp32 (vector path)")
+    compare(run_prefill(b), ref_prefill(b), "f32", "f32 prefill")
+
+
+def test_last_row_matches_decode_at_the_same_length():
+    b = written(chunk_batch([90], [40], [W.RT], seed=33))
+    got = oracle.widen(run_prefill(b), "bf16")[-1]
+    ref = oracle.decode(b.q_prefill[-1:], b.k_pool, b.v_pool, b.block_tables[:1], b.dir[:1], b.ctx_lens[:1], "bf16")[0]
+    assert np.abs(got - ref).max() <= 2e-2

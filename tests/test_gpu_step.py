@@ -1,0 +1,35 @@
+"""One whole mixed step (kv_write -> prefill -> decode) through MixedStep, the
+dispatch the benchmark times, on the full mixed-step workload, against the
+oracle's step; with and without the prefill on a side stream."""
+
+import numpy as np
+import pytest
+
+from paper_2504_09590_amd import workload as W
+from tests.gpu_helpers import announce, compare, oracle_step, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def mixed():
+    b = W.generate(3)
+    return b, oracle_step(b)
+
+
+@pytest.mark.parametrize("overlap", [False, True])
+def test_mixed_step_full(mixed, overlap):
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    from paper_2504_09590_amd.step import MixedStep
+    b, (k1, v1, pre_ref, dec_ref) = mixed
+    dev = bros.to_device(b)
+    step = MixedStep(b, dev, overlap=overlap)
+    announce(f"mixed step {b.name} overlap={overlap}")
+    pre, dec = step.run()
+    torch.cuda.synchronize()
+    for name, ref, got in (("k", k1, dev.k_pool), ("v", v1, dev.v_pool)):
+        assert np.array_equal(bros.to_host_bits(got), ref), f"{name} pool after the step"
+    mx_p, mean_p = compare(bros.to_host_bits(pre), pre_ref, "bf16", "step prefill")
+    mx_d, mean_d = compare(bros.to_host_bits(dec), dec_ref, "bf16", "step decode")
+    print(f"step prefill max {mx_p:.3g} mean {mean_p:.3g}; decode max {mx_d:.3g} mean {mean_d:.3g}")
