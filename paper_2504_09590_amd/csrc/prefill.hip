@@ -45,9 +45,11 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_ca
 template <int G>
 __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(PrefillArgs a) {
   constexpr int QT = 128 / G;   // positions per tile
-  __shared__ __attribute__((aligned(16))) uint8_t s_k[kKeys * kKRow];
-  __shared__ __attribute__((aligned(16))) uint8_t s_vt[kHeadDim * kVRow];
-  __shared__ __attribute__((aligned(16))) int s_kpos[kKeys];
+  // Two LDS buffers: tile kt is read from buffer kt % 2 while tile kt + 1,
+  // already fetched into registers, is staged into the other one.
+  __shared__ __attribute__((aligned(16))) uint8_t s_k[2][kKeys * kKRow];
+  __shared__ __attribute__((aligned(16))) uint8_t s_vt[2][kHeadDim * kVRow];
+  __shared__ __attribute__((aligned(16))) int s_kpos[2][kKeys];
 
   // XCD-aware order: consecutive workgroup ids land on different XCDs (id % 8),
   // so give each XCD a contiguous run of work items. The tiles of one
@@ -109,9 +111,12 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(PrefillArgs a) {
   const int slot = tid >> 4;   // staging: thread copies slot `slot`, dims [8*dc, 8*dc+8) of each block
   const int dc = tid & 15;
 
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    uint4 kreg[4], vreg[4];
-    int kp[4];
+  // Global -> registers for tile kt: thread copies slot `slot`, dims
+  // [8*dc, 8*dc+8) of each of the tile's four blocks (each block's tile is
+  // 4 KiB contiguous, so a wave's load instruction reads 1 KiB contiguous).
+  uint4 kreg[4], vreg[4];
+  int kp[4];
+  auto fetch = [&](int kt) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int b = kt * 4 + u;
@@ -128,19 +133,36 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(PrefillArgs a) {
       }
       kp[u] = valid ? pos : INT_MAX;
     }
+  };
+  // Registers -> LDS buffer `buf`: K row-major, V transposed, key positions.
+  auto stage = [&](int buf) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int key = u * kBlockSize + slot;
-      *reinterpret_cast<uint4*>(s_k + key * kKRow + dc * 16) = kreg[u];
+      *reinterpret_cast<uint4*>(s_k[buf] + key * kKRow + dc * 16) = kreg[u];
       const uint32_t w4[4] = {vreg[u].x, vreg[u].y, vreg[u].z, vreg[u].w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const uint16_t val = (uint16_t)((e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xffffu));
-        *reinterpret_cast<uint16_t*>(s_vt + (8 * dc + e) * kVRow + key * 2) = val;
+        *reinterpret_cast<uint16_t*>(s_vt[buf] + (8 * dc + e) * kVRow + key * 2) = val;
       }
-      if (dc == 0) s_kpos[key] = kp[u];
+      if (dc == 0) s_kpos[buf][key] = kp[u];
     }
-    __syncthreads();
+  };
+
+  if (n_tiles > 0) {
+    fetch(0);
+    stage(0);
+  }
+  __syncthreads();
+
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    const int buf = kt & 1;
+    const bool more = kt + 1 < n_tiles;
+    if (more) fetch(kt + 1);   // in flight while this tile is computed
+    const uint8_t* sk = s_k[buf];
+    const uint8_t* svt = s_vt[buf];
+    const int* skpos = s_kpos[buf];
 
     // S^T = K Q^T for keys [32*st, 32*st + 32).
     floatx16 sacc[2];
@@ -149,7 +171,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(PrefillArgs a) {
       sacc[st] = floatx16{};
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
-        const uint4 kv = *reinterpret_cast<const uint4*>(s_k + (32 * st + mrow) * kKRow + (16 * c + 8 * half) * 2);
+        const uint4 kv = *reinterpret_cast<const uint4*>(sk + (32 * st + mrow) * kKRow + (16 * c + 8 * half) * 2);
         sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[c], sacc[st], 0, 0, 0);
       }
     }
@@ -161,7 +183,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(PrefillArgs a) {
     for (int st = 0; st < 2; ++st) {
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        const int4 kp4 = *reinterpret_cast<const int4*>(s_kpos + 32 * st + 8 * jq + 4 * half);
+        const int4 kp4 = *reinterpret_cast<const int4*>(skpos + 32 * st + 8 * jq + 4 * half);
         const int kpv[4] = {kp4.x, kp4.y, kp4.z, kp4.w};
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
@@ -210,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(PrefillArgs a) {
     // 16c2 + 8 + 4*half + {0..3}, the same permutation the P operand carries.
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      const uint8_t* vrow = s_vt + (32 * dt + mrow) * kVRow;
+      const uint8_t* vrow = svt + (32 * dt + mrow) * kVRow;
 #pragma unroll
       for (int c2 = 0; c2 < 4; ++c2) {
         const uint2 lo = *reinterpret_cast<const uint2*>(vrow + (16 * c2 + 4 * half) * 2);
@@ -219,6 +241,9 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(PrefillArgs a) {
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pf[c2], o[dt], 0, 0, 0);
       }
     }
+    // The other buffer was last read in the previous iteration, before the
+    // barrier that ended it, so it can be overwritten now.
+    if (more) stage(buf ^ 1);
     __syncthreads();
   }
 
