@@ -166,7 +166,8 @@ int bros_attn_decode(void* out, const void* q,
  *   workspace    : at least bros_attn_workspace_size(BROS_WS_PREFILL, dtype,
  *                  num_q_tokens, num_q_heads, head_dim, max_ctx) bytes.
  * bf16 runs the QK^T and PV products on the matrix cores (P is rounded to bf16
- * before PV); fp32 runs a vector-ALU path.
+ * before PV) for max_ctx <= 32768; fp32, and bf16 beyond that context, run a
+ * vector-ALU path that needs the workspace the size query reports.
  */
 int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
                             int32_t num_q_tokens, int32_t max_q_len,

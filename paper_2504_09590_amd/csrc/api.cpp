@@ -83,7 +83,9 @@ size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
   if (num_rows <= 0 || num_q_heads <= 0 || head_dim != 128 || max_ctx < 0) return 0;
   if (dtype != BROS_F32 && dtype != BROS_BF16) return 0;
   if (kind == BROS_WS_DECODE) return bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx);
-  if (kind == BROS_WS_PREFILL) return dtype == BROS_BF16 ? 0 : bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx);
+  if (kind == BROS_WS_PREFILL)
+    return (dtype == BROS_BF16 && max_ctx <= bros::kPrefillMaxCtxMfma) ? 0
+                                                                    : bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx);
   return 0;
 }
 
@@ -160,7 +162,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const float scale_log2 = resolve_scale(scale, head_dim);
 
-  if (dtype == BROS_BF16) {
+  if (dtype == BROS_BF16 && max_ctx <= bros::kPrefillMaxCtxMfma) {
     bros::PrefillArgs a{};
     a.out = out;
     a.q = q;
@@ -186,7 +188,8 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
     return launch_status(fn, bros::launch_prefill_mfma(a, group, (int)total, s));
   }
 
-  // fp32: every prefill row is a decode row with its own causal context.
+  // fp32 (and bf16 beyond the matrix-core path's context limit): every prefill
+  // row is a decode row with its own causal context.
   const size_t need = bros::decode_workspace_bytes(num_q_tokens, num_q_heads, max_ctx);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 16)))
     return fail(BROS_E_WORKSPACE, "%s: workspace of %zu bytes (16-byte aligned) required, got %zu at %p", fn, need, workspace_bytes, workspace);
@@ -213,7 +216,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   a.split_blocks = plan.split_blocks;
   a.n_split_max = plan.n_split_max;
   a.scale_log2 = scale_log2;
-  return launch_status(fn, bros::launch_decode(a, group, false, s));
+  return launch_status(fn, bros::launch_decode(a, group, dtype == BROS_BF16, s));
 }
 
 }  // extern "C"

@@ -83,6 +83,9 @@ size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max
 
 hipError_t launch_kv_write(const KvWriteArgs& a, bool bf16, hipStream_t stream);
 hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream);
+// Longest context the matrix-core prefill handles (its block table is staged
+// whole in LDS); longer contexts take the vector path.
+constexpr int32_t kPrefillMaxCtxMfma = 32768;
 hipError_t launch_prefill_mfma(const PrefillArgs& a, int group, int num_tiles_total, hipStream_t stream);
 int prefill_positions_per_tile(int group);
 
