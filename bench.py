@@ -149,29 +149,34 @@ def main():
     K = args.steps
     ev = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
           for k in ("kv_write", "prefill", "decode")}
+    written = [torch.cuda.Event() for _ in range(K)]
+    prefilled = [torch.cuda.Event() for _ in range(K)]
+    side = step.side if step.overlap else stream
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
     for i in range(K):
-        if args.overlap:
-            step.run()
-        else:
-            a, b = ev["kv_write"][i]
-            a.record(stream); step.kv_write(stream); b.record(stream)
-            a, b = ev["prefill"][i]
-            a.record(stream); step.prefill(stream); b.record(stream)
-            a, b = ev["decode"][i]
-            a.record(stream); step.decode(stream); b.record(stream)
+        # one step: kv_write, then prefill (on the side stream when overlapping) and decode;
+        # every call is bracketed by events on the stream it runs on
+        a, b = ev["kv_write"][i]
+        a.record(stream); step.kv_write(stream); b.record(stream)
+        if step.overlap:
+            written[i].record(stream)
+            side.wait_event(written[i])
+        a, b = ev["prefill"][i]
+        a.record(side); step.prefill(side); b.record(side)
+        a, b = ev["decode"][i]
+        a.record(stream); step.decode(stream); b.record(stream)
+        if step.overlap:
+            prefilled[i].record(side)
+            stream.wait_event(prefilled[i])
     end.record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall) * 1e3
     ms = start.elapsed_time(end) / K
 
-    per_call = {}
-    if not args.overlap:
-        for k, pairs in ev.items():
-            per_call[k] = float(np.mean([a.elapsed_time(b) for a, b in pairs]))
+    per_call = {k: float(np.mean([a.elapsed_time(b) for a, b in pairs])) for k, pairs in ev.items()}
 
     dec_ms = per_call.get("decode")
     roof = None
@@ -192,7 +197,7 @@ def main():
                    "prefill_chunks": batch.num_prefill, "decode_rows": batch.num_seqs - batch.num_prefill,
                    "q_heads": batch.num_q_heads, "kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim,
                    "block_size": 16, "pool_blocks": batch.num_blocks, "sum_ctx": int(batch.ctx_lens.sum()),
-                   "overlap": bool(args.overlap)},
+                   "overlap": bool(step.overlap)},
         "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
         "step_bytes": work["step_bytes"],
         "roofline": roof,

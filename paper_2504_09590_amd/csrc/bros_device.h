@@ -40,16 +40,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // Base-2 exponential on the transcendental unit (exp2(-inf) = 0).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Sum over the 16 lanes of a DPP row; every lane of the row receives the total.
-// Butterfly: swap neighbours, swap pairs, mirror halves of 8, mirror the row.
-__device__ __forceinline__ float row16_sum(float x) {
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0xb1, 0xf, 0xf, false);   // quad_perm [1,0,3,2]
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x4e, 0xf, 0xf, false);   // quad_perm [2,3,0,1]
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x141, 0xf, 0xf, false);  // row_half_mirror
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x140, 0xf, 0xf, false);  // row_mirror
-  return x;
-}
-
 __device__ __forceinline__ int wave_id_uniform() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
 }
