@@ -116,9 +116,12 @@ template <> struct Frag<true> {
   }
   __device__ void zero() { w[0] = w[1] = w[2] = w[3] = 0u; }
   __device__ float dot(const Frag& k) const {
-    float acc = 0.0f;
+    // First pair in the three-operand form with an inline zero addend: the
+    // builtin with a 0 addend becomes the tied-accumulator form plus a move.
+    float acc;
+    asm("v_dot2_f32_bf16 %0, %1, %2, 0" : "=v"(acc) : "v"(w[0]), "v"(k.w[0]));
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 1; i < 4; ++i)
       acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w[i]), __builtin_bit_cast(bf16x2_t, k.w[i]), acc, false);
     return acc;
   }
@@ -147,6 +150,14 @@ template <bool BF16>
 __device__ __forceinline__ void store_out(void* out, size_t elem, float v) {
   if constexpr (BF16) static_cast<uint16_t*>(out)[elem] = (uint16_t)f32_to_bf16_bits(v);
   else static_cast<float*>(out)[elem] = v;
+}
+
+// Lane id through an asm the compiler cannot hoist: values derived from it are
+// recomputed where they are used instead of being held in registers.
+__device__ __forceinline__ int lane_id_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
 }
 
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {   // round to nearest even
@@ -359,6 +370,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
   __shared__ float s_acc[kWaves][GW][kHeadDim];
   __shared__ float s_m[kWaves][GW], s_l[kWaves][GW];
   __shared__ int s_scan[kThreads];
+  __shared__ v4u_t s_q[kWaves][GW][16];   // bf16: each wave's query fragments, re-read per block
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -425,6 +437,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
     const int nb = it.split < it.nsp ? max(0, min(it.nblk, it.b_begin + SB) - it.b_begin) : 0;
     it.nbw = nb > stream ? (nb - stream + NSTREAM - 1) / NSTREAM : 0;
     it.dirv = seq_direction(a.dir, a.cls, it.s);
+    // Every field but the table entry is the same on all lanes: keep them in
+    // scalar registers so the vector registers go to KV fragments.
+    it.row = __builtin_amdgcn_readfirstlane(it.row);
+    it.s = __builtin_amdgcn_readfirstlane(it.s);
+    it.g = __builtin_amdgcn_readfirstlane(it.g);
+    it.split = __builtin_amdgcn_readfirstlane(it.split);
+    it.ctx = __builtin_amdgcn_readfirstlane(it.ctx);
+    it.nblk = __builtin_amdgcn_readfirstlane(it.nblk);
+    it.nsp = __builtin_amdgcn_readfirstlane(it.nsp);
+    it.b_begin = __builtin_amdgcn_readfirstlane(it.b_begin);
+    it.nbw = __builtin_amdgcn_readfirstlane(it.nbw);
+    it.dirv = __builtin_amdgcn_readfirstlane(it.dirv);
     it.tbl = -1;
     if (lane < nb) it.tbl = a.block_tables[(size_t)it.s * a.max_blocks_per_seq + it.b_begin + lane];
   };
@@ -432,9 +456,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
   Frag<BF16> q[GW];
   Frag<BF16> kf[4], vf[4];
   WaveState<GW, BF16> st;
-  int vbase = 0;
-#pragma unroll
-  for (int k = 0; k < LY::NHALVE; ++k) vbase += stage_side(C, k) * (LY::NV >> (k + 1));
   const bool primary = (C & (LY::DUP - 1)) == 0;
   const size_t lane_off = (size_t)R * kHeadDim + 8 * C;
 
@@ -480,6 +501,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
     const int h0 = cur.g * G + hh * GW;   // first query head of this wave
 #pragma unroll
     for (int h = 0; h < GW; ++h) q[h].load(a.q, ((size_t)cur.row * Hq + h0 + h) * kHeadDim + 8 * C);
+    if constexpr (BF16) {   // park the query in LDS: its registers are free between blocks
+      if (R == 0) {
+#pragma unroll
+        for (int h = 0; h < GW; ++h) s_q[w][h][C] = v4u_t{q[h].w[0], q[h].w[1], q[h].w[2], q[h].w[3]};
+      }
+    }
     st.reset();
 
     for (int i = 0; i < cur.nbw; ++i) {
@@ -488,21 +515,37 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
       const bool more_here = i + 1 < cur.nbw;
       const bool more_next = !more_here && nxt_ok && nxt.nbw > 0;
       float sc[LY::NPL];
-      if (blk >= 0) st.scores(q, kf, a.scale_log2, C, sc);
+      if (blk >= 0) {
+        if constexpr (BF16) {
+          int cq = C;
+          asm volatile("" : "+v"(cq));   // keeps the reads in the loop (not hoisted into registers)
+#pragma unroll
+          for (int h = 0; h < GW; ++h) {
+            const v4u_t v = s_q[w][h][cq];
+            q[h].w[0] = v.x; q[h].w[1] = v.y; q[h].w[2] = v.z; q[h].w[3] = v.w;
+          }
+        }
+        st.scores(q, kf, a.scale_log2, C, sc);
+      }
       // K registers are free: request the next block's keys
       if (more_here) blk_next = issue_k(cur, i + 1);
       else if (more_next) blk_next = issue_k(nxt, 0);
       else blk_next = -1;
       if (blk >= 0) {
         if (b == cur.nblk - 1 && (cur.ctx & (kBlockSize - 1)) != 0) {   // tail: drop slots past the context
+          const int lt = lane_id_here();
+          const int Rt = lt >> 4, Ct = lt & 15;
+          int vbase = 0;   // index v = 4 * head + j of this lane's first score
+#pragma unroll
+          for (int k = 0; k < LY::NHALVE; ++k) vbase += stage_side(Ct, k) * (LY::NV >> (k + 1));
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            if (b * kBlockSize + slot_of_offset(R + 4 * j, cur.dirv) >= cur.ctx) vf[j].zero();
+            if (b * kBlockSize + slot_of_offset(Rt + 4 * j, cur.dirv) >= cur.ctx) vf[j].zero();
           }
 #pragma unroll
           for (int i2 = 0; i2 < LY::NPL; ++i2) {
             const int j = (vbase + i2) & 3;
-            if (b * kBlockSize + slot_of_offset(R + 4 * j, cur.dirv) >= cur.ctx) sc[i2] = -INFINITY;
+            if (b * kBlockSize + slot_of_offset(Rt + 4 * j, cur.dirv) >= cur.ctx) sc[i2] = -INFINITY;
           }
         }
         st.update(sc, vf, primary);
