@@ -21,7 +21,8 @@
 // the next block's K is requested as soon as this block's scores are formed,
 // its V as soon as this block's PV product is done; the next block may belong
 // to the workgroup's next item, so the memory pipeline does not drain between
-// items. KV tiles are read with non-temporal loads (they are used once).
+// items. KV tiles are read with non-temporal loads when one wave uses them;
+// when two waves share a tile (G = 8) the loads stay cacheable.
 //
 // Per block, within each 16-lane row (one DPP row):
 //   1. QK partials over the lane's 8 dims for its 4 slots x GW heads (dot2 on
@@ -359,6 +360,85 @@ struct Item {
   int tbl;   // per lane: table entry of block b_begin + lane (or -1)
 };
 
+// Items per row (KV heads x splits) and their prefix, row-major and within a
+// row KV-head-major, in LDS when the rows fit. Returns the number of items, or
+// the size of a padded item space (empty items skipped) when they do not.
+__device__ int build_item_prefix(const DecodeArgs& a, int* s_prefix, int* s_scan) {
+  const int tid = threadIdx.x;
+  const int nkv = a.num_kv_heads;
+  if (a.num_rows > kMaxRowsLds) return a.num_rows * nkv * a.n_split_max;
+  const int per = (a.num_rows + kThreads - 1) / kThreads;
+  const int r0 = tid * per;
+  int mine = 0;
+  for (int r = r0; r < min(a.num_rows, r0 + per); ++r) {
+    int s, ctx;
+    resolve_row(a, r, s, ctx);
+    mine += nkv * splits_of(ctx, a.split_blocks);
+  }
+  s_scan[tid] = mine;
+  __syncthreads();
+  for (int off = 1; off < kThreads; off <<= 1) {   // inclusive scan of the per-thread sums
+    const int v = tid >= off ? s_scan[tid - off] : 0;
+    __syncthreads();
+    s_scan[tid] += v;
+    __syncthreads();
+  }
+  int run = s_scan[tid] - mine;
+  for (int r = r0; r < min(a.num_rows, r0 + per); ++r) {
+    s_prefix[r] = run;
+    int s, ctx;
+    resolve_row(a, r, s, ctx);
+    run += nkv * splits_of(ctx, a.split_blocks);
+  }
+  if (tid == kThreads - 1) s_prefix[a.num_rows] = s_scan[kThreads - 1];
+  __syncthreads();
+  return s_prefix[a.num_rows];
+}
+
+// Item k as stream `stream` of NSTREAM sees it: its blocks are b_begin + stream,
+// b_begin + stream + NSTREAM, ... (nbw of them); lane i holds the table entry of
+// block b_begin + i.
+template <int NSTREAM>
+__device__ __forceinline__ void fetch_item(const DecodeArgs& a, const int* s_prefix, int k, int stream,
+                                           int lane, Item& it) {
+  const int nkv = a.num_kv_heads;
+  const int SB = a.split_blocks;
+  const bool use_prefix = a.num_rows <= kMaxRowsLds;
+  int row, local;
+  if (use_prefix) {
+    row = upper_index(s_prefix, a.num_rows + 1, k);
+    local = k - s_prefix[row];
+  } else {
+    row = k / (nkv * a.n_split_max);
+    local = k - row * nkv * a.n_split_max;
+  }
+  it.row = row;
+  resolve_row(a, row, it.s, it.ctx);
+  it.nsp = splits_of(it.ctx, SB);
+  const int per_g = use_prefix ? it.nsp : a.n_split_max;
+  it.g = local / per_g;
+  it.split = local - it.g * per_g;
+  it.nblk = it.ctx > 0 ? (it.ctx + kBlockSize - 1) / kBlockSize : 0;
+  it.b_begin = it.split * SB;
+  const int nb = it.split < it.nsp ? max(0, min(it.nblk, it.b_begin + SB) - it.b_begin) : 0;
+  it.nbw = nb > stream ? (nb - stream + NSTREAM - 1) / NSTREAM : 0;
+  it.dirv = seq_direction(a.dir, a.cls, it.s);
+  // Every field but the table entry is the same on all lanes: keep them in
+  // scalar registers so the vector registers go to KV fragments.
+  it.row = __builtin_amdgcn_readfirstlane(it.row);
+  it.s = __builtin_amdgcn_readfirstlane(it.s);
+  it.g = __builtin_amdgcn_readfirstlane(it.g);
+  it.split = __builtin_amdgcn_readfirstlane(it.split);
+  it.ctx = __builtin_amdgcn_readfirstlane(it.ctx);
+  it.nblk = __builtin_amdgcn_readfirstlane(it.nblk);
+  it.nsp = __builtin_amdgcn_readfirstlane(it.nsp);
+  it.b_begin = __builtin_amdgcn_readfirstlane(it.b_begin);
+  it.nbw = __builtin_amdgcn_readfirstlane(it.nbw);
+  it.dirv = __builtin_amdgcn_readfirstlane(it.dirv);
+  it.tbl = -1;
+  if (lane < nb) it.tbl = a.block_tables[(size_t)it.s * a.max_blocks_per_seq + it.b_begin + lane];
+}
+
 template <int G, bool BF16>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ? 4 : 1))) void decode_kernel(DecodeArgs a) {
   constexpr int GW = G > 4 ? 4 : G;     // heads per wave
@@ -379,79 +459,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
   const int C = lane & 15;
   const int stream = w / HS;
   const int hh = w % HS;                 // which four heads of the group this wave owns
-  const int SB = a.split_blocks;
   const int nkv = a.num_kv_heads;
   const int Hq = a.num_q_heads;
 
-  // Items per row and their prefix (row-major; within a row, KV head-major).
-  const bool use_prefix = a.num_rows <= kMaxRowsLds;
-  int total;
-  if (use_prefix) {
-    const int per = (a.num_rows + kThreads - 1) / kThreads;
-    const int r0 = tid * per;
-    int mine = 0;
-    for (int r = r0; r < min(a.num_rows, r0 + per); ++r) {
-      int s, ctx;
-      resolve_row(a, r, s, ctx);
-      mine += nkv * splits_of(ctx, SB);
-    }
-    s_scan[tid] = mine;
-    __syncthreads();
-    for (int off = 1; off < kThreads; off <<= 1) {   // inclusive scan of the per-thread sums
-      const int v = tid >= off ? s_scan[tid - off] : 0;
-      __syncthreads();
-      s_scan[tid] += v;
-      __syncthreads();
-    }
-    int run = s_scan[tid] - mine;
-    for (int r = r0; r < min(a.num_rows, r0 + per); ++r) {
-      s_prefix[r] = run;
-      int s, ctx;
-      resolve_row(a, r, s, ctx);
-      run += nkv * splits_of(ctx, SB);
-    }
-    if (tid == kThreads - 1) s_prefix[a.num_rows] = s_scan[kThreads - 1];
-    __syncthreads();
-    total = s_prefix[a.num_rows];
-  } else {
-    total = a.num_rows * nkv * a.n_split_max;   // padded space; empty items are skipped
-  }
-
-  auto fetch = [&](int k, Item& it) {
-    int row, local;
-    if (use_prefix) {
-      row = upper_index(s_prefix, a.num_rows + 1, k);
-      local = k - s_prefix[row];
-    } else {
-      row = k / (nkv * a.n_split_max);
-      local = k - row * nkv * a.n_split_max;
-    }
-    it.row = row;
-    resolve_row(a, row, it.s, it.ctx);
-    it.nsp = splits_of(it.ctx, SB);
-    const int per_g = use_prefix ? it.nsp : a.n_split_max;
-    it.g = local / per_g;
-    it.split = local - it.g * per_g;
-    it.nblk = it.ctx > 0 ? (it.ctx + kBlockSize - 1) / kBlockSize : 0;
-    it.b_begin = it.split * SB;
-    const int nb = it.split < it.nsp ? max(0, min(it.nblk, it.b_begin + SB) - it.b_begin) : 0;
-    it.nbw = nb > stream ? (nb - stream + NSTREAM - 1) / NSTREAM : 0;
-    it.dirv = seq_direction(a.dir, a.cls, it.s);
-    // Every field but the table entry is the same on all lanes: keep them in
-    // scalar registers so the vector registers go to KV fragments.
-    it.row = __builtin_amdgcn_readfirstlane(it.row);
-    it.s = __builtin_amdgcn_readfirstlane(it.s);
-    it.g = __builtin_amdgcn_readfirstlane(it.g);
-    it.split = __builtin_amdgcn_readfirstlane(it.split);
-    it.ctx = __builtin_amdgcn_readfirstlane(it.ctx);
-    it.nblk = __builtin_amdgcn_readfirstlane(it.nblk);
-    it.nsp = __builtin_amdgcn_readfirstlane(it.nsp);
-    it.b_begin = __builtin_amdgcn_readfirstlane(it.b_begin);
-    it.nbw = __builtin_amdgcn_readfirstlane(it.nbw);
-    it.dirv = __builtin_amdgcn_readfirstlane(it.dirv);
-    it.tbl = -1;
-    if (lane < nb) it.tbl = a.block_tables[(size_t)it.s * a.max_blocks_per_seq + it.b_begin + lane];
-  };
+  const int total = build_item_prefix(a, s_prefix, s_scan);
+  auto fetch = [&](int k, Item& it) { fetch_item<NSTREAM>(a, s_prefix, k, stream, lane, it); };
 
   Frag<BF16> q[GW];
   Frag<BF16> kf[4], vf[4];
@@ -464,7 +476,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
     if (blk < 0 || blk >= a.num_blocks) return -1;
     const size_t base = ((size_t)blk * nkv + it.g) * kTileElems + lane_off;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) kf[j].load_stream(a.k_pool, base + (size_t)(4 * j) * kHeadDim);
+    for (int j = 0; j < 4; ++j) {
+      // With two waves per stream both read the same tile: keep it cacheable so
+      // the second read is served on chip.
+      if constexpr (HS == 1) kf[j].load_stream(a.k_pool, base + (size_t)(4 * j) * kHeadDim);
+      else kf[j].load(a.k_pool, base + (size_t)(4 * j) * kHeadDim);
+    }
     return blk;
   };
   auto issue_v = [&](const Item& it, int i) {
@@ -472,7 +489,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
     if (blk < 0 || blk >= a.num_blocks) return;
     const size_t base = ((size_t)blk * nkv + it.g) * kTileElems + lane_off;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) vf[j].load_stream(a.v_pool, base + (size_t)(4 * j) * kHeadDim);
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (HS == 1) vf[j].load_stream(a.v_pool, base + (size_t)(4 * j) * kHeadDim);
+      else vf[j].load(a.v_pool, base + (size_t)(4 * j) * kHeadDim);
+    }
   };
 
   int k = blockIdx.x;
@@ -613,6 +633,226 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BF16 ?
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 decode on the matrix cores. Per 16-slot block of one (row, KV head), the
+// G query heads of the group form a dense 16 x G x 128 contraction:
+//   S^T[slot][head] = K[slot][:] . q[head][:]     mfma 16x16x32 (N = heads, padded)
+//   O^T[dim][head] += V^T[dim][slot] P^T[slot][head]   mfma 16x16x16
+// Lane l = 16 grp + col. In the C layout of the first product lane l holds the
+// scores of slots 4 grp .. 4 grp + 3 for head col, which is exactly the B layout
+// the second product wants for P^T: the softmax weights never move between
+// lanes. The contraction index of the first product is a permutation of the
+// head dims (K and q use the same one), and row m of output tile t is dim
+// 8 m + t, so every operand comes from plain 16-byte loads: K slot col, dims
+// 32 c + 8 grp ..; V slots 4 grp + j, dims 8 col ..; and lane l ends up holding
+// dims 32 grp .. 32 grp + 31 of head col. Lanes with col >= G compute padding
+// that is never stored.
+// ---------------------------------------------------------------------------
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
+
+__device__ __forceinline__ v4u_t load_nt(const void* base, size_t elem) {
+  return __builtin_nontemporal_load(reinterpret_cast<const v4u_t*>(static_cast<const uint16_t*>(base) + elem));
+}
+
+template <int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void decode_mfma_kernel(DecodeArgs a) {
+  static_assert(G >= 1 && G <= 16, "heads of a group must fit the 16 MFMA columns");
+  constexpr int NSTREAM = kWaves;   // every wave is a block stream of the item
+
+  __shared__ int s_prefix[kMaxRowsLds + 1];
+  __shared__ int s_scan[kThreads];
+  __shared__ float s_acc[kWaves][G][kHeadDim];
+  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int stream = wave_id_uniform();
+  const int grp = lane >> 4;
+  const int col = lane & 15;
+  const bool head_lane = col < G;
+  const int nkv = a.num_kv_heads;
+  const int Hq = a.num_q_heads;
+
+  const int total = build_item_prefix(a, s_prefix, s_scan);
+
+  const uint32_t k_lane = (uint32_t)col * kHeadDim + 8 * grp;        // + 32 c
+  const uint32_t v_lane = (uint32_t)(4 * grp) * kHeadDim + 8 * col;  // + j * kHeadDim
+  v4u_t qf[4], kf[4], vf[4];
+  floatx4_t acc[8];
+  float m_ref, l_part;
+
+  auto issue_k = [&](const Item& it, int i) -> int {
+    const int blk = read_lane_i32(it.tbl, stream + NSTREAM * i);
+    if (blk < 0 || blk >= a.num_blocks) return -1;
+    const size_t base = ((size_t)blk * nkv + it.g) * kTileElems + k_lane;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) kf[c] = load_nt(a.k_pool, base + 32 * c);
+    return blk;
+  };
+  auto issue_v = [&](const Item& it, int i) {
+    const int blk = read_lane_i32(it.tbl, stream + NSTREAM * i);
+    if (blk < 0 || blk >= a.num_blocks) return;
+    const size_t base = ((size_t)blk * nkv + it.g) * kTileElems + v_lane;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) vf[j] = load_nt(a.v_pool, base + (size_t)j * kHeadDim);
+  };
+
+  int k = blockIdx.x;
+  Item cur, nxt;
+  bool cur_ok = false;
+  while (k < total) {   // first non-empty item (only the padded space has empties)
+    fetch_item<NSTREAM>(a, s_prefix, k, stream, lane, cur);
+    if (cur.split < cur.nsp) { cur_ok = true; break; }
+    k += gridDim.x;
+  }
+  int blk_next = -1;
+  if (cur_ok && cur.nbw > 0) {
+    blk_next = issue_k(cur, 0);
+    issue_v(cur, 0);
+  }
+
+  while (cur_ok) {
+    int kn = k + gridDim.x;
+    bool nxt_ok = false;
+    while (kn < total) {
+      fetch_item<NSTREAM>(a, s_prefix, kn, stream, lane, nxt);
+      if (nxt.split < nxt.nsp) { nxt_ok = true; break; }
+      kn += gridDim.x;
+    }
+    {
+      const size_t qoff = ((size_t)cur.row * Hq + cur.g * G + col) * kHeadDim + 8 * grp;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        qf[c] = v4u_t{0u, 0u, 0u, 0u};
+        if (head_lane) qf[c] = *reinterpret_cast<const v4u_t*>(static_cast<const uint16_t*>(a.q) + qoff + 32 * c);
+      }
+    }
+    m_ref = kNoMax;
+    l_part = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[t] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    for (int i = 0; i < cur.nbw; ++i) {
+      const int blk = blk_next;
+      const int b = cur.b_begin + stream + NSTREAM * i;   // logical block index
+      const bool more_here = i + 1 < cur.nbw;
+      const bool more_next = !more_here && nxt_ok && nxt.nbw > 0;
+      floatx4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (blk >= 0) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[c]),
+                                                       __builtin_bit_cast(bf16x8_t, qf[c]), sc, 0, 0, 0);
+      }
+      // K registers are free: request the next block's keys
+      if (more_here) blk_next = issue_k(cur, i + 1);
+      else if (more_next) blk_next = issue_k(nxt, 0);
+      else blk_next = -1;
+      if (blk >= 0) {
+        float s[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s[r] = sc[r] * a.scale_log2;
+        if (b == cur.nblk - 1 && (cur.ctx & (kBlockSize - 1)) != 0) {   // tail: drop slots past the context
+          const int gt = lane_id_here() >> 4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (b * kBlockSize + slot_of_offset(4 * gt + r, cur.dirv) >= cur.ctx) {
+              s[r] = -INFINITY;
+              vf[r] = v4u_t{0u, 0u, 0u, 0u};
+            }
+          }
+        }
+        float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+        if (__builtin_amdgcn_ballot_w64(head_lane && mx > m_ref + kRescaleSlack) != 0) {
+          // rare: move the reference max of each head to the max over its 16 slots
+          mx = fmaxf(mx, __shfl_xor(mx, 16));
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          const float m_new = fmaxf(m_ref, mx);
+          const float alpha = fast_exp2(m_ref - m_new);
+          m_ref = m_new;
+          l_part *= alpha;
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[t][r] *= alpha;
+          }
+        }
+        float p[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) p[r] = fast_exp2(s[r] - m_ref);
+        l_part += (p[0] + p[1]) + (p[2] + p[3]);
+        const short4_t pb = __builtin_bit_cast(short4_t, uint2{pack2_bf16(p[0], p[1]), pack2_bf16(p[2], p[3])});
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const uint32_t sel = (t & 1) ? 0x07060302u : 0x05040100u;
+          const uint32_t lo = __builtin_amdgcn_perm(vf[1][t >> 1], vf[0][t >> 1], sel);
+          const uint32_t hi = __builtin_amdgcn_perm(vf[3][t >> 1], vf[2][t >> 1], sel);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, uint2{lo, hi}), pb, acc[t], 0, 0, 0);
+        }
+      }
+      // V registers are free: request the next block's values
+      if (more_here) issue_v(cur, i + 1);
+      else if (more_next) issue_v(nxt, 0);
+    }
+
+    // The four lane groups of a head hold disjoint slots: total their weights.
+    float l_head = l_part;
+    l_head += __shfl_xor(l_head, 16);
+    l_head += __shfl_xor(l_head, 32);
+    if (head_lane) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float* dst = &s_acc[stream][col][32 * grp + 8 * r];
+        *reinterpret_cast<floatx4_t*>(dst) = floatx4_t{acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+        *reinterpret_cast<floatx4_t*>(dst + 4) = floatx4_t{acc[4][r], acc[5][r], acc[6][r], acc[7][r]};
+      }
+      if (grp == 0) {
+        s_m[stream][col] = m_ref;
+        s_l[stream][col] = l_head;
+      }
+    }
+    __syncthreads();
+    // Combine the streams and write this item's result (or split partial).
+    const int hbase = cur.g * G;
+    for (int idx = tid; idx < G * kHeadDim; idx += kThreads) {
+      const int h = idx / kHeadDim;
+      const int d = idx - h * kHeadDim;
+      float M = kNoMax;
+#pragma unroll
+      for (int sidx = 0; sidx < NSTREAM; ++sidx) M = fmaxf(M, s_m[sidx][h]);
+      float L = 0.0f, A = 0.0f;
+#pragma unroll
+      for (int sidx = 0; sidx < NSTREAM; ++sidx) {
+        const float wt = fast_exp2(s_m[sidx][h] - M);
+        L = fmaf(s_l[sidx][h], wt, L);
+        A = fmaf(s_acc[sidx][h][d], wt, A);
+      }
+      const size_t qh = (size_t)cur.row * Hq + hbase + h;
+      if (cur.nsp == 1) {
+        store_out<true>(a.out, qh * kHeadDim + d, L > 0.0f ? A / L : 0.0f);
+      } else {
+        const size_t slot = qh * a.n_split_max + cur.split;
+        a.ws_acc[slot * kHeadDim + d] = A;
+        if (d == 0) {
+          a.ws_ml[2 * slot] = M;
+          a.ws_ml[2 * slot + 1] = L;
+        }
+      }
+    }
+    __syncthreads();
+
+    if (!nxt_ok) break;
+    if (cur.nbw == 0 && nxt.nbw > 0) {   // nothing was in flight for the next item yet
+      blk_next = issue_k(nxt, 0);
+      issue_v(nxt, 0);
+    }
+    cur = nxt;
+    k = kn;
+  }
+}
+
 // Combine the split partials of every (row, head) whose context needed more
 // than one split: o = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i.
 template <bool BF16>
@@ -659,10 +899,15 @@ int resident_workgroups(const void* kernel, int slot) {
 template <int G, bool BF16>
 hipError_t launch_group(const DecodeArgs& a, hipStream_t stream, int slot) {
   const long long padded = (long long)a.num_rows * a.num_kv_heads * a.n_split_max;
-  const int resident = resident_workgroups(reinterpret_cast<const void*>(&decode_kernel<G, BF16>), slot);
+  const void* kern = BF16 ? reinterpret_cast<const void*>(&decode_mfma_kernel<G>)
+                          : reinterpret_cast<const void*>(&decode_kernel<G, false>);
+  const int resident = resident_workgroups(kern, slot);
   const int grid = (int)(padded < resident ? padded : resident);
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL((decode_kernel<G, BF16>), dim3(grid), dim3(kThreads), 0, stream, a);
+  if constexpr (BF16)
+    hipLaunchKernelGGL((decode_mfma_kernel<G>), dim3(grid), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<G, false>), dim3(grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_split_max <= 1) return e;
   hipLaunchKernelGGL((decode_merge_kernel<BF16>), dim3((unsigned)(a.num_rows * a.num_q_heads)),
