@@ -135,8 +135,16 @@ int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
  *   scale        : softmax scale; <= 0 selects 1 / sqrt(head_dim)
  *   workspace    : device scratch of at least
  *                  bros_attn_workspace_size(BROS_WS_DECODE, dtype, num_seqs,
- *                  num_q_heads, head_dim, max_ctx) bytes (may be NULL when that
- *                  size is 0). Holds split-K partial results; overwritten.
+ *                  num_q_heads, head_dim, max_ctx) bytes, 16-byte aligned (may
+ *                  be NULL when that size is 0); overwritten by every call.
+ *                  bf16: the first tile of each row and the partial results
+ *                  of (row, KV head) contexts shared by several workers (the
+ *                  grid's waves each take an equal share of the 16-slot
+ *                  tiles); its size does not depend on max_ctx. fp32: split-K
+ *                  partials, needed only when a context spans several splits.
+ *                  Two calls that share a workspace must not overlap in time.
+ * Errors: BROS_E_SHAPE also when bf16 num_seqs * num_kv_heads *
+ * ceil(max_ctx / 16) exceeds 2^31 - 1.
  */
 int bros_attn_decode(void* out, const void* q,
                      const void* k_pool, const void* v_pool, int32_t num_blocks,
@@ -181,8 +189,9 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
 
 /*
  * Bytes of device workspace the call `kind` needs for `num_rows` query rows
- * (num_seqs for decode, num_q_tokens for prefill). Pure host arithmetic.
- * Returns 0 for unsupported arguments.
+ * (num_seqs for decode, num_q_tokens for prefill). Pure host arithmetic; it
+ * does not know num_kv_heads and sizes bf16 decode for groups of up to 8
+ * query heads. Returns 0 for unsupported arguments.
  */
 size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
                                 int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);

@@ -82,10 +82,10 @@ size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
                                 int32_t num_q_heads, int32_t head_dim, int32_t max_ctx) {
   if (num_rows <= 0 || num_q_heads <= 0 || head_dim != 128 || max_ctx < 0) return 0;
   if (dtype != BROS_F32 && dtype != BROS_BF16) return 0;
-  if (kind == BROS_WS_DECODE) return bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx);
+  const bool bf16 = dtype == BROS_BF16;
+  if (kind == BROS_WS_DECODE) return bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx, bf16);
   if (kind == BROS_WS_PREFILL)
-    return (dtype == BROS_BF16 && max_ctx <= bros::kPrefillMaxCtxMfma) ? 0
-                                                                    : bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx);
+    return (bf16 && max_ctx <= bros::kPrefillMaxCtxMfma) ? 0 : bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx, bf16);
   return 0;
 }
 
@@ -108,7 +108,10 @@ int bros_attn_decode(void* out, const void* q,
   if (st) return st;
   if (!aligned(out, 16) || !aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16))
     return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
-  const size_t need = bros::decode_workspace_bytes(num_seqs, num_q_heads, max_ctx);
+  const bool bf16 = dtype == BROS_BF16;
+  if (bf16 && (long long)num_seqs * num_kv_heads * ((max_ctx + 15) / 16) > 0x7fffffffLL)
+    return fail(BROS_E_SHAPE, "%s: more than 2^31 (row, KV head, block) tiles", fn);
+  const size_t need = bros::decode_workspace_bytes(num_seqs, num_q_heads, max_ctx, bf16);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 16)))
     return fail(BROS_E_WORKSPACE, "%s: workspace of %zu bytes (16-byte aligned) required, got %zu at %p", fn, need, workspace_bytes, workspace);
   const bros::DecodePlan plan = bros::plan_decode(num_seqs, max_ctx);
@@ -122,8 +125,6 @@ int bros_attn_decode(void* out, const void* q,
   a.cls = cls;
   a.ctx_lens = ctx_lens;
   a.cu_q = nullptr;
-  a.ws_acc = static_cast<float*>(workspace);
-  a.ws_ml = need > 0 ? static_cast<float*>(workspace) + (size_t)num_seqs * num_q_heads * plan.n_split_max * head_dim : nullptr;
   a.num_rows = num_seqs;
   a.num_seqs = num_seqs;
   a.num_blocks = num_blocks;
@@ -134,7 +135,8 @@ int bros_attn_decode(void* out, const void* q,
   a.split_blocks = plan.split_blocks;
   a.n_split_max = plan.n_split_max;
   a.scale_log2 = resolve_scale(scale, head_dim);
-  return launch_status(fn, bros::launch_decode(a, group, dtype == BROS_BF16, static_cast<hipStream_t>(stream)));
+  bros::set_decode_workspace(a, need > 0 ? workspace : nullptr, bf16);
+  return launch_status(fn, bros::launch_decode(a, group, bf16, static_cast<hipStream_t>(stream)));
 }
 
 int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
@@ -190,7 +192,10 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
 
   // fp32 (and bf16 beyond the matrix-core path's context limit): every prefill
   // row is a decode row with its own causal context.
-  const size_t need = bros::decode_workspace_bytes(num_q_tokens, num_q_heads, max_ctx);
+  const bool bf16 = dtype == BROS_BF16;
+  if (bf16 && (long long)num_q_tokens * num_kv_heads * ((max_ctx + 15) / 16) > 0x7fffffffLL)
+    return fail(BROS_E_SHAPE, "%s: more than 2^31 (row, KV head, block) tiles", fn);
+  const size_t need = bros::decode_workspace_bytes(num_q_tokens, num_q_heads, max_ctx, bf16);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 16)))
     return fail(BROS_E_WORKSPACE, "%s: workspace of %zu bytes (16-byte aligned) required, got %zu at %p", fn, need, workspace_bytes, workspace);
   const bros::DecodePlan plan = bros::plan_decode(num_q_tokens, max_ctx);
@@ -204,8 +209,6 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   a.cls = cls;
   a.ctx_lens = ctx_lens;
   a.cu_q = cu_q;
-  a.ws_acc = static_cast<float*>(workspace);
-  a.ws_ml = need > 0 ? static_cast<float*>(workspace) + (size_t)num_q_tokens * num_q_heads * plan.n_split_max * head_dim : nullptr;
   a.num_rows = num_q_tokens;
   a.num_seqs = num_seqs;
   a.num_blocks = num_blocks;
@@ -216,7 +219,8 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   a.split_blocks = plan.split_blocks;
   a.n_split_max = plan.n_split_max;
   a.scale_log2 = scale_log2;
-  return launch_status(fn, bros::launch_decode(a, group, dtype == BROS_BF16, s));
+  bros::set_decode_workspace(a, need > 0 ? workspace : nullptr, bf16);
+  return launch_status(fn, bros::launch_decode(a, group, bf16, s));
 }
 
 }  // extern "C"

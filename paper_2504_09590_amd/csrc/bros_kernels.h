@@ -38,8 +38,13 @@ struct DecodeArgs {
   const uint8_t* cls;
   const int32_t* ctx_lens;
   const int32_t* cu_q;
-  float* ws_acc;          // [rows][Hq][n_split_max][D] unnormalised partial outputs
-  float* ws_ml;           // [rows][Hq][n_split_max][2] (running max in log2 units, sum)
+  // Partial results. fp32 split-K: [rows][Hq][n_split_max] slots. bf16 (one
+  // worker per wave over an even share of the tiles): slot (row * Hkv + g +
+  // worker) * G + head-in-group, for segments cut between workers.
+  float* ws_acc;          // [slots][D] unnormalised partial outputs
+  float* ws_ml;           // [slots][2] (running max in log2 units, sum)
+  int32_t* ws_rows;       // bf16: first tile of each row, [rows + 1]
+  int32_t num_workers;    // bf16: waves of the grid (workers beyond the tile count idle)
   int32_t num_rows;
   int32_t num_seqs;
   int32_t num_blocks;
@@ -79,7 +84,10 @@ struct DecodePlan {
   int32_t n_split_max;
 };
 DecodePlan plan_decode(int32_t num_rows, int32_t max_ctx);
-size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max_ctx);
+size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max_ctx, bool bf16);
+// Points the workspace fields of `a` (num_rows, num_q_heads, n_split_max set)
+// into `ws`, laid out as decode_workspace_bytes sized it.
+void set_decode_workspace(DecodeArgs& a, void* ws, bool bf16);
 
 hipError_t launch_kv_write(const KvWriteArgs& a, bool bf16, hipStream_t stream);
 hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream);

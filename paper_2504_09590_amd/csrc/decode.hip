@@ -656,201 +656,370 @@ __device__ __forceinline__ v4u_t load_nt(const void* base, size_t elem) {
   return __builtin_nontemporal_load(reinterpret_cast<const v4u_t*>(static_cast<const uint16_t*>(base) + elem));
 }
 
+typedef const int32_t __attribute__((address_space(4)))* scalar_i32_ptr;
+
+// A wave-uniform int32 read through the scalar cache (read-only data only).
+__device__ __forceinline__ int32_t load_uniform(const int32_t* p, size_t i) {
+  return ((scalar_i32_ptr)p)[i];   // address-space cast: C-style only
+}
+
+// Tiles of one row: KV heads x blocks of its visible context.
+__device__ __forceinline__ int row_tiles(const DecodeArgs& a, int row) {
+  int s, ctx;
+  resolve_row(a, row, s, ctx);
+  return ctx > 0 ? a.num_kv_heads * ((ctx + kBlockSize - 1) / kBlockSize) : 0;
+}
+
+// Prefix of tiles over rows in LDS: entry c is the first tile of row c * chunk
+// (chunk = 1 up to kMaxRowsLds rows). Workgroup 0 also stores the per-row
+// prefix in the workspace for the merge kernel. Returns the total tile count.
+__device__ int build_tile_prefix(const DecodeArgs& a, int* s_pre, int* s_scan, int chunk, int nch) {
+  const int tid = threadIdx.x;
+  const int per = (nch + kThreads - 1) / kThreads;   // chunks per thread
+  const int c0 = tid * per;
+  int mine = 0;
+  for (int c = c0; c < min(nch, c0 + per); ++c)
+    for (int r = c * chunk; r < min(a.num_rows, (c + 1) * chunk); ++r) mine += row_tiles(a, r);
+  s_scan[tid] = mine;
+  __syncthreads();
+  for (int off = 1; off < kThreads; off <<= 1) {
+    const int v = tid >= off ? s_scan[tid - off] : 0;
+    __syncthreads();
+    s_scan[tid] += v;
+    __syncthreads();
+  }
+  int run = s_scan[tid] - mine;
+  for (int c = c0; c < min(nch, c0 + per); ++c) {
+    s_pre[c] = run;
+    for (int r = c * chunk; r < min(a.num_rows, (c + 1) * chunk); ++r) {
+      if (blockIdx.x == 0) a.ws_rows[r] = run;
+      run += row_tiles(a, r);
+    }
+  }
+  if (tid == kThreads - 1) {
+    s_pre[nch] = s_scan[kThreads - 1];
+    if (blockIdx.x == 0) a.ws_rows[a.num_rows] = s_scan[kThreads - 1];
+  }
+  __syncthreads();
+  return s_pre[nch];
+}
+
+// Where a worker stands: tile b of (row, KV head g). All fields are uniform.
+struct Cursor {
+  int row, s, ctx, nblk, dirv, g, b;
+};
+
+__device__ __forceinline__ void enter_row(const DecodeArgs& a, int row, Cursor& c) {
+  c.row = row;
+  resolve_row(a, row, c.s, c.ctx);
+  c.nblk = c.ctx > 0 ? (c.ctx + kBlockSize - 1) / kBlockSize : 0;
+  c.dirv = seq_direction(a.dir, a.cls, c.s);
+  c.row = __builtin_amdgcn_readfirstlane(c.row);
+  c.s = __builtin_amdgcn_readfirstlane(c.s);
+  c.ctx = __builtin_amdgcn_readfirstlane(c.ctx);
+  c.nblk = __builtin_amdgcn_readfirstlane(c.nblk);
+  c.dirv = __builtin_amdgcn_readfirstlane(c.dirv);
+}
+
+// Next tile in (row, KV head, block) order; rows without context have no tiles.
+// Only called while tiles remain in the worker's range, so a row exists.
+__device__ __forceinline__ void advance(const DecodeArgs& a, Cursor& c) {
+  if (++c.b < c.nblk) return;
+  c.b = 0;
+  if (++c.g < a.num_kv_heads) return;
+  c.g = 0;
+  int row = c.row;
+  do {
+    ++row;
+    enter_row(a, row, c);
+  } while (c.nblk == 0 && row + 1 < a.num_rows);
+}
+
+// Tile t (< total): binary search over the chunk prefix, then rows of the chunk.
+__device__ void locate(const DecodeArgs& a, const int* s_pre, int chunk, int nch, int t, Cursor& c) {
+  int ch = upper_index(s_pre, nch + 1, t);
+  ch = min(ch, nch - 1);
+  int base = s_pre[ch];
+  int row = ch * chunk;
+  for (;;) {
+    enter_row(a, row, c);
+    const int n = c.nblk * a.num_kv_heads;
+    if (t < base + n || row + 1 >= a.num_rows) break;
+    base += n;
+    ++row;
+  }
+  const int local = t - base;
+  c.g = __builtin_amdgcn_readfirstlane(c.nblk > 0 ? local / c.nblk : 0);
+  c.b = __builtin_amdgcn_readfirstlane(local - c.g * c.nblk);
+}
+
+__device__ __forceinline__ int worker_of(int64_t tile, int64_t total, int64_t workers) {
+  return (int)(((tile + 1) * workers - 1) / total);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
 template <int G>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void decode_mfma_kernel(DecodeArgs a) {
   static_assert(G >= 1 && G <= 16, "heads of a group must fit the 16 MFMA columns");
-  constexpr int NSTREAM = kWaves;   // every wave is a block stream of the item
-
-  __shared__ int s_prefix[kMaxRowsLds + 1];
+  __shared__ int s_pre[kMaxRowsLds + 1];
   __shared__ int s_scan[kThreads];
-  __shared__ float s_acc[kWaves][G][kHeadDim];
-  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int stream = wave_id_uniform();
   const int grp = lane >> 4;
   const int col = lane & 15;
   const bool head_lane = col < G;
   const int nkv = a.num_kv_heads;
   const int Hq = a.num_q_heads;
 
-  const int total = build_item_prefix(a, s_prefix, s_scan);
+  const int chunk = (a.num_rows + kMaxRowsLds - 1) / kMaxRowsLds;
+  const int nch = (a.num_rows + chunk - 1) / chunk;
+  const int total = build_tile_prefix(a, s_pre, s_scan, chunk, nch);
+
+  // This wave's share of the tiles; with fewer tiles than waves the last waves
+  // idle, so every worker has at least one tile.
+  const int workers = min(a.num_workers, total);
+  const int wid = blockIdx.x * kWaves + wave_id_uniform();
+  if (wid >= workers) return;
+  const int t0 = (int)((int64_t)wid * total / workers);
+  const int t1 = (int)((int64_t)(wid + 1) * total / workers);
+  const int n = t1 - t0;
 
   const uint32_t k_lane = (uint32_t)col * kHeadDim + 8 * grp;        // + 32 c
   const uint32_t v_lane = (uint32_t)(4 * grp) * kHeadDim + 8 * col;  // + j * kHeadDim
   v4u_t qf[4], kf[4], vf[4];
   floatx4_t acc[8];
-  float m_ref, l_part;
+  float m_ref = kNoMax, l_part = 0.0f;
 
-  auto issue_k = [&](const Item& it, int i) -> int {
-    const int blk = read_lane_i32(it.tbl, stream + NSTREAM * i);
-    if (blk < 0 || blk >= a.num_blocks) return -1;
-    const size_t base = ((size_t)blk * nkv + it.g) * kTileElems + k_lane;
+  auto table = [&](const Cursor& c) -> int {
+    const int blk = load_uniform(a.block_tables, (size_t)c.s * a.max_blocks_per_seq + c.b);
+    return (blk >= 0 && blk < a.num_blocks) ? blk : -1;
+  };
+  auto issue_k = [&](int blk, int g) {
+    if (blk < 0) return;
+    const size_t base = ((size_t)blk * nkv + g) * kTileElems + k_lane;
 #pragma unroll
     for (int c = 0; c < 4; ++c) kf[c] = load_nt(a.k_pool, base + 32 * c);
-    return blk;
   };
-  auto issue_v = [&](const Item& it, int i) {
-    const int blk = read_lane_i32(it.tbl, stream + NSTREAM * i);
-    if (blk < 0 || blk >= a.num_blocks) return;
-    const size_t base = ((size_t)blk * nkv + it.g) * kTileElems + v_lane;
+  auto issue_v = [&](int blk, int g) {
+    if (blk < 0) return;
+    const size_t base = ((size_t)blk * nkv + g) * kTileElems + v_lane;
 #pragma unroll
     for (int j = 0; j < 4; ++j) vf[j] = load_nt(a.v_pool, base + (size_t)j * kHeadDim);
   };
-
-  int k = blockIdx.x;
-  Item cur, nxt;
-  bool cur_ok = false;
-  while (k < total) {   // first non-empty item (only the padded space has empties)
-    fetch_item<NSTREAM>(a, s_prefix, k, stream, lane, cur);
-    if (cur.split < cur.nsp) { cur_ok = true; break; }
-    k += gridDim.x;
-  }
-  int blk_next = -1;
-  if (cur_ok && cur.nbw > 0) {
-    blk_next = issue_k(cur, 0);
-    issue_v(cur, 0);
-  }
-
-  while (cur_ok) {
-    int kn = k + gridDim.x;
-    bool nxt_ok = false;
-    while (kn < total) {
-      fetch_item<NSTREAM>(a, s_prefix, kn, stream, lane, nxt);
-      if (nxt.split < nxt.nsp) { nxt_ok = true; break; }
-      kn += gridDim.x;
+  auto load_q = [&](const Cursor& c) {
+    const size_t qoff = ((size_t)c.row * Hq + c.g * G + col) * kHeadDim + 8 * grp;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      qf[k] = v4u_t{0u, 0u, 0u, 0u};
+      if (head_lane) qf[k] = *reinterpret_cast<const v4u_t*>(static_cast<const uint16_t*>(a.q) + qoff + 32 * k);
     }
-    {
-      const size_t qoff = ((size_t)cur.row * Hq + cur.g * G + col) * kHeadDim + 8 * grp;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        qf[c] = v4u_t{0u, 0u, 0u, 0u};
-        if (head_lane) qf[c] = *reinterpret_cast<const v4u_t*>(static_cast<const uint16_t*>(a.q) + qoff + 32 * c);
-      }
-    }
-    m_ref = kNoMax;
-    l_part = 0.0f;
-#pragma unroll
-    for (int t = 0; t < 8; ++t) acc[t] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  };
 
-    for (int i = 0; i < cur.nbw; ++i) {
-      const int blk = blk_next;
-      const int b = cur.b_begin + stream + NSTREAM * i;   // logical block index
-      const bool more_here = i + 1 < cur.nbw;
-      const bool more_next = !more_here && nxt_ok && nxt.nbw > 0;
-      floatx4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
-      if (blk >= 0) {
+  Cursor c0, c1;
+  locate(a, s_pre, chunk, nch, t0, c0);
+  int blk0 = table(c0);
+  issue_k(blk0, c0.g);
+  issue_v(blk0, c0.g);
+  load_q(c0);
+  bool whole = c0.b == 0;   // this wave saw the segment's first tile
+  c1 = c0;
+  int blk1 = -1;
+  if (n > 1) {
+    advance(a, c1);
+    blk1 = table(c1);
+  }
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[c]),
-                                                       __builtin_bit_cast(bf16x8_t, qf[c]), sc, 0, 0, 0);
-      }
-      // K registers are free: request the next block's keys
-      if (more_here) blk_next = issue_k(cur, i + 1);
-      else if (more_next) blk_next = issue_k(nxt, 0);
-      else blk_next = -1;
-      if (blk >= 0) {
-        float s[4];
+  for (int t = 0; t < 8; ++t) acc[t] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+  for (int i = 0; i < n; ++i) {
+    // the tile after next: its table entry is read now, used one tile later
+    Cursor c2 = c1;
+    int blk2 = -1;
+    if (i + 2 < n) {
+      advance(a, c2);
+      blk2 = table(c2);
+    }
+    floatx4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (blk0 >= 0) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) s[r] = sc[r] * a.scale_log2;
-        if (b == cur.nblk - 1 && (cur.ctx & (kBlockSize - 1)) != 0) {   // tail: drop slots past the context
-          const int gt = lane_id_here() >> 4;
+      for (int k = 0; k < 4; ++k)
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[k]),
+                                                     __builtin_bit_cast(bf16x8_t, qf[k]), sc, 0, 0, 0);
+    }
+    const bool seg_end = c0.b == c0.nblk - 1 || i + 1 == n;
+    // K and query registers are free: the next tile's keys (and query on a new segment)
+    if (i + 1 < n) {
+      issue_k(blk1, c1.g);
+      if (seg_end) load_q(c1);
+    }
+    if (blk0 >= 0) {
+      float s[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            if (b * kBlockSize + slot_of_offset(4 * gt + r, cur.dirv) >= cur.ctx) {
-              s[r] = -INFINITY;
-              vf[r] = v4u_t{0u, 0u, 0u, 0u};
-            }
+      for (int r = 0; r < 4; ++r) s[r] = sc[r] * a.scale_log2;
+      if (c0.b == c0.nblk - 1 && (c0.ctx & (kBlockSize - 1)) != 0) {   // tail: drop slots past the context
+        const int gt = lane_id_here() >> 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (c0.b * kBlockSize + slot_of_offset(4 * gt + r, c0.dirv) >= c0.ctx) {
+            s[r] = -INFINITY;
+            vf[r] = v4u_t{0u, 0u, 0u, 0u};
           }
         }
-        float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-        if (__builtin_amdgcn_ballot_w64(head_lane && mx > m_ref + kRescaleSlack) != 0) {
-          // rare: move the reference max of each head to the max over its 16 slots
-          mx = fmaxf(mx, __shfl_xor(mx, 16));
-          mx = fmaxf(mx, __shfl_xor(mx, 32));
-          const float m_new = fmaxf(m_ref, mx);
-          const float alpha = fast_exp2(m_ref - m_new);
-          m_ref = m_new;
-          l_part *= alpha;
-#pragma unroll
-          for (int t = 0; t < 8; ++t) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) acc[t][r] *= alpha;
-          }
-        }
-        float p[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) p[r] = fast_exp2(s[r] - m_ref);
-        l_part += (p[0] + p[1]) + (p[2] + p[3]);
-        const short4_t pb = __builtin_bit_cast(short4_t, uint2{pack2_bf16(p[0], p[1]), pack2_bf16(p[2], p[3])});
+      }
+      float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+      if (__builtin_amdgcn_ballot_w64(head_lane && mx > m_ref + kRescaleSlack) != 0) {
+        // rare: move each head's reference max to the max over its 16 slots
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_ref, mx);
+        const float alpha = fast_exp2(m_ref - m_new);
+        m_ref = m_new;
+        l_part *= alpha;
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-          const uint32_t sel = (t & 1) ? 0x07060302u : 0x05040100u;
-          const uint32_t lo = __builtin_amdgcn_perm(vf[1][t >> 1], vf[0][t >> 1], sel);
-          const uint32_t hi = __builtin_amdgcn_perm(vf[3][t >> 1], vf[2][t >> 1], sel);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, uint2{lo, hi}), pb, acc[t], 0, 0, 0);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[t][r] *= alpha;
         }
       }
-      // V registers are free: request the next block's values
-      if (more_here) issue_v(cur, i + 1);
-      else if (more_next) issue_v(nxt, 0);
+      float p[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) p[r] = fast_exp2(s[r] - m_ref);
+      l_part += (p[0] + p[1]) + (p[2] + p[3]);
+      const short4_t pb = __builtin_bit_cast(short4_t, uint2{pack2_bf16(p[0], p[1]), pack2_bf16(p[2], p[3])});
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint32_t sel = (t & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t lo = __builtin_amdgcn_perm(vf[1][t >> 1], vf[0][t >> 1], sel);
+        const uint32_t hi = __builtin_amdgcn_perm(vf[3][t >> 1], vf[2][t >> 1], sel);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, uint2{lo, hi}), pb, acc[t], 0, 0, 0);
+      }
     }
+    // V registers are free: the next tile's values
+    if (i + 1 < n) issue_v(blk1, c1.g);
 
-    // The four lane groups of a head hold disjoint slots: total their weights.
-    float l_head = l_part;
-    l_head += __shfl_xor(l_head, 16);
-    l_head += __shfl_xor(l_head, 32);
-    if (head_lane) {
+    if (seg_end) {
+      // The four lane groups of a head hold disjoint slots: total their weights.
+      float l_head = l_part;
+      l_head += __shfl_xor(l_head, 16);
+      l_head += __shfl_xor(l_head, 32);
+      const bool direct = whole && c0.b == c0.nblk - 1;   // the whole segment was this wave's
+      if (head_lane) {
+        const int h = c0.g * G + col;
+        if (direct) {
+          const float inv = l_head > 0.0f ? 1.0f / l_head : 0.0f;
+          uint16_t* o = static_cast<uint16_t*>(a.out) + ((size_t)c0.row * Hq + h) * kHeadDim + 32 * grp;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float* dst = &s_acc[stream][col][32 * grp + 8 * r];
-        *reinterpret_cast<floatx4_t*>(dst) = floatx4_t{acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
-        *reinterpret_cast<floatx4_t*>(dst + 4) = floatx4_t{acc[4][r], acc[5][r], acc[6][r], acc[7][r]};
-      }
-      if (grp == 0) {
-        s_m[stream][col] = m_ref;
-        s_l[stream][col] = l_head;
-      }
-    }
-    __syncthreads();
-    // Combine the streams and write this item's result (or split partial).
-    const int hbase = cur.g * G;
-    for (int idx = tid; idx < G * kHeadDim; idx += kThreads) {
-      const int h = idx / kHeadDim;
-      const int d = idx - h * kHeadDim;
-      float M = kNoMax;
+          for (int r = 0; r < 4; ++r) {
+            const v4u_t w4 = v4u_t{pack2_bf16(acc[0][r] * inv, acc[1][r] * inv), pack2_bf16(acc[2][r] * inv, acc[3][r] * inv),
+                                   pack2_bf16(acc[4][r] * inv, acc[5][r] * inv), pack2_bf16(acc[6][r] * inv, acc[7][r] * inv)};
+            *reinterpret_cast<v4u_t*>(o + 8 * r) = w4;
+          }
+        } else {
+          const size_t slot = ((size_t)c0.row * nkv + c0.g + wid) * G + col;   // partial (segment + worker)
+          float* dst = a.ws_acc + slot * kHeadDim + 32 * grp;
 #pragma unroll
-      for (int sidx = 0; sidx < NSTREAM; ++sidx) M = fmaxf(M, s_m[sidx][h]);
-      float L = 0.0f, A = 0.0f;
-#pragma unroll
-      for (int sidx = 0; sidx < NSTREAM; ++sidx) {
-        const float wt = fast_exp2(s_m[sidx][h] - M);
-        L = fmaf(s_l[sidx][h], wt, L);
-        A = fmaf(s_acc[sidx][h][d], wt, A);
-      }
-      const size_t qh = (size_t)cur.row * Hq + hbase + h;
-      if (cur.nsp == 1) {
-        store_out<true>(a.out, qh * kHeadDim + d, L > 0.0f ? A / L : 0.0f);
-      } else {
-        const size_t slot = qh * a.n_split_max + cur.split;
-        a.ws_acc[slot * kHeadDim + d] = A;
-        if (d == 0) {
-          a.ws_ml[2 * slot] = M;
-          a.ws_ml[2 * slot + 1] = L;
+          for (int r = 0; r < 4; ++r) {
+            *reinterpret_cast<floatx4_t*>(dst + 8 * r) = floatx4_t{acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+            *reinterpret_cast<floatx4_t*>(dst + 8 * r + 4) = floatx4_t{acc[4][r], acc[5][r], acc[6][r], acc[7][r]};
+          }
+          if (grp == 0) {
+            a.ws_ml[2 * slot] = m_ref;
+            a.ws_ml[2 * slot + 1] = l_head;
+          }
         }
       }
+      m_ref = kNoMax;
+      l_part = 0.0f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) acc[t] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      whole = true;
     }
-    __syncthreads();
-
-    if (!nxt_ok) break;
-    if (cur.nbw == 0 && nxt.nbw > 0) {   // nothing was in flight for the next item yet
-      blk_next = issue_k(nxt, 0);
-      issue_v(nxt, 0);
-    }
-    cur = nxt;
-    k = kn;
+    c0 = c1;
+    blk0 = blk1;
+    c1 = c2;
+    blk1 = blk2;
   }
+}
+
+// Rows whose (row, KV head) segment was cut between workers: combine the
+// partials o = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w. Rows without
+// context get zeros; segments a single worker covered were written directly.
+// One wave per (row, query head): lanes take 64 partials' (m, l) at a time,
+// then every lane folds two head dims over the partials with eight loads in
+// flight. (Merging inside the decode kernel instead would need device-scope
+// release/acquire between workgroups, which on this chip writes back and
+// invalidates a whole L2 per segment; the kernel boundary is far cheaper.)
+constexpr int kMergeWaves = 4;
+
+__global__ __launch_bounds__(kMergeWaves * kWave) void decode_mfma_merge_kernel(DecodeArgs a, int group) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int item = blockIdx.x * kMergeWaves + wave_id_uniform();
+  if (item >= a.num_rows * a.num_q_heads) return;
+  const int hq = item % a.num_q_heads;
+  const int row = item / a.num_q_heads;
+  const int g = hq / group, hl = hq - g * group;
+  int s, ctx;
+  resolve_row(a, row, s, ctx);
+  uint32_t* out = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.out) + ((size_t)row * a.num_q_heads + hq) * kHeadDim) + lane;
+  if (ctx <= 0) {
+    *out = 0u;
+    return;
+  }
+  const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
+  const int total = a.ws_rows[a.num_rows];
+  const int workers = min(a.num_workers, total);
+  const int64_t first_tile = (int64_t)a.ws_rows[row] + (int64_t)g * nblk;
+  const int w0 = __builtin_amdgcn_readfirstlane(worker_of(first_tile, total, workers));
+  const int w1 = __builtin_amdgcn_readfirstlane(worker_of(first_tile + nblk - 1, total, workers));
+  if (w0 == w1) return;
+  const size_t seg = (size_t)row * a.num_kv_heads + g;
+
+  float M = kNoMax;
+  for (int c = w0; c <= w1; c += kWave) {
+    const int w = c + lane;
+    if (w <= w1) M = fmaxf(M, a.ws_ml[2 * ((seg + w) * group + hl)]);
+  }
+  M = wave_max(M);
+  float L = 0.0f, Ax = 0.0f, Ay = 0.0f;
+  for (int c = w0; c <= w1; c += kWave) {
+    const int w = c + lane;
+    float wt = 0.0f;
+    if (w <= w1) {
+      const size_t slot = (seg + w) * group + hl;
+      wt = fast_exp2(a.ws_ml[2 * slot] - M);
+      L = fmaf(a.ws_ml[2 * slot + 1], wt, L);
+    }
+    const int cnt = min(kWave, w1 - c + 1);
+    for (int j0 = 0; j0 < cnt; j0 += 8) {
+      float2 v[8];
+      float wj[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {   // indices clamped in range; padding gets weight 0
+        const int j = min(j0 + u, cnt - 1);
+        wj[u] = (j0 + u < cnt) ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wt), j)) : 0.0f;
+        v[u] = reinterpret_cast<const float2*>(a.ws_acc + ((seg + c + j) * group + hl) * kHeadDim)[lane];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        Ax = fmaf(v[u].x, wj[u], Ax);
+        Ay = fmaf(v[u].y, wj[u], Ay);
+      }
+    }
+  }
+  L = wave_sum(L);
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  *out = pack2_bf16(Ax * inv, Ay * inv);
 }
 
 // Combine the split partials of every (row, head) whose context needed more
@@ -896,23 +1065,34 @@ int resident_workgroups(const void* kernel, int slot) {
   return cache[dev][slot];
 }
 
+// Workgroups of the bf16 decode grid at most (four workers each): what 256
+// compute units hold at four waves per SIMD. The workspace is sized for it.
+constexpr int kMaxDecodeGrid = 1024;
+
 template <int G, bool BF16>
-hipError_t launch_group(const DecodeArgs& a, hipStream_t stream, int slot) {
-  const long long padded = (long long)a.num_rows * a.num_kv_heads * a.n_split_max;
-  const void* kern = BF16 ? reinterpret_cast<const void*>(&decode_mfma_kernel<G>)
-                          : reinterpret_cast<const void*>(&decode_kernel<G, false>);
-  const int resident = resident_workgroups(kern, slot);
-  const int grid = (int)(padded < resident ? padded : resident);
-  if (grid <= 0) return hipSuccess;
-  if constexpr (BF16)
+hipError_t launch_group(DecodeArgs a, hipStream_t stream, int slot) {
+  if constexpr (BF16) {
+    int grid = resident_workgroups(reinterpret_cast<const void*>(&decode_mfma_kernel<G>), slot);
+    grid = grid < kMaxDecodeGrid ? grid : kMaxDecodeGrid;
+    a.num_workers = grid * kWaves;
     hipLaunchKernelGGL((decode_mfma_kernel<G>), dim3(grid), dim3(kThreads), 0, stream, a);
-  else
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned merge_grid = (unsigned)(((long long)a.num_rows * a.num_q_heads + kMergeWaves - 1) / kMergeWaves);
+    hipLaunchKernelGGL(decode_mfma_merge_kernel, dim3(merge_grid), dim3(kMergeWaves * kWave), 0, stream, a, G);
+    return hipGetLastError();
+  } else {
+    const long long padded = (long long)a.num_rows * a.num_kv_heads * a.n_split_max;
+    const int resident = resident_workgroups(reinterpret_cast<const void*>(&decode_kernel<G, false>), slot);
+    const int grid = (int)(padded < resident ? padded : resident);
+    if (grid <= 0) return hipSuccess;
     hipLaunchKernelGGL((decode_kernel<G, false>), dim3(grid), dim3(kThreads), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.n_split_max <= 1) return e;
-  hipLaunchKernelGGL((decode_merge_kernel<BF16>), dim3((unsigned)(a.num_rows * a.num_q_heads)),
-                     dim3(kHeadDim), 0, stream, a);
-  return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.n_split_max <= 1) return e;
+    hipLaunchKernelGGL((decode_merge_kernel<false>), dim3((unsigned)(a.num_rows * a.num_q_heads)),
+                       dim3(kHeadDim), 0, stream, a);
+    return hipGetLastError();
+  }
 }
 
 }  // namespace
@@ -927,11 +1107,34 @@ DecodePlan plan_decode(int32_t num_rows, int32_t max_ctx) {
   return p;
 }
 
-size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max_ctx) {
+static size_t round_up_256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max_ctx, bool bf16) {
+  if (bf16) {
+    const int gmax = num_q_heads < 8 ? num_q_heads : 8;
+    const size_t slots = (size_t)num_rows * num_q_heads + (size_t)kWaves * kMaxDecodeGrid * gmax;
+    return round_up_256(((size_t)num_rows + 1) * sizeof(int32_t)) + round_up_256(slots * kHeadDim * sizeof(float)) +
+           slots * 2 * sizeof(float);
+  }
   const DecodePlan p = plan_decode(num_rows, max_ctx);
   if (p.n_split_max <= 1) return 0;
   const size_t slots = (size_t)num_rows * num_q_heads * p.n_split_max;
   return slots * kHeadDim * sizeof(float) + slots * 2 * sizeof(float);
+}
+
+void set_decode_workspace(DecodeArgs& a, void* ws, bool bf16) {
+  char* base = static_cast<char*>(ws);
+  if (bf16) {
+    const int gmax = a.num_q_heads < 8 ? a.num_q_heads : 8;
+    const size_t slots = (size_t)a.num_rows * a.num_q_heads + (size_t)kWaves * kMaxDecodeGrid * gmax;
+    a.ws_rows = reinterpret_cast<int32_t*>(base);
+    a.ws_acc = reinterpret_cast<float*>(base + round_up_256(((size_t)a.num_rows + 1) * sizeof(int32_t)));
+    a.ws_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(a.ws_acc) + round_up_256(slots * kHeadDim * sizeof(float)));
+    return;
+  }
+  a.ws_rows = nullptr;
+  a.ws_acc = reinterpret_cast<float*>(base);
+  a.ws_ml = base ? a.ws_acc + (size_t)a.num_rows * a.num_q_heads * a.n_split_max * kHeadDim : nullptr;
 }
 
 hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream) {

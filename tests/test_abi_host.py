@@ -112,10 +112,13 @@ def test_prefill_rejects():
 
 def test_workspace_query():
     q = bros.bros_attn_workspace_size
-    assert q(0, 1, 4, 8, 128, 64) == 0              # single split: no workspace
+    assert q(0, 0, 4, 8, 128, 64) == 0              # fp32, single split: no workspace
+    assert q(0, 0, 64, 32, 128, 8192) > 0           # fp32, several splits
+    small = q(0, 1, 4, 8, 128, 64)                  # bf16: row prefix + per-worker partials, any length
     big = q(0, 1, 64, 32, 128, 8192)
-    assert big > 0 and big % 16 == 0
-    assert q(0, 1, 64, 32, 128, 16384) >= big
+    assert 0 < small < big and big % 16 == 0
+    assert q(0, 1, 64, 32, 128, 16384) == big       # bf16 size does not grow with the context
+    assert q(0, 1, 65, 32, 128, 8192) > big
     assert q(1, 1, 2048, 32, 128, 8192) == 0        # bf16 prefill runs on the matrix cores, no scratch
     assert q(1, 0, 2048, 32, 128, 8192) > 0
     assert q(0, 1, 4, 8, 64, 64) == 0               # unsupported head_dim
