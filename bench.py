@@ -35,12 +35,13 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
 METRIC = "µs per mixed RT/BE attention step + achieved KV GB/s (% of HBM peak)"
 
 # HBM traffic of the decode call from rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, one
-# counter per run, KiB per dispatch, summed over decode_kernel and decode_merge_kernel).
+# counter per run, KiB per dispatch, summed over decode_mfma_kernel and decode_mfma_merge_kernel).
 # The counters are scaled by what they read for a plain 1 GiB device copy
 # (--calibrate-copy): FETCH_SIZE reads half the bytes copied, WRITE_SIZE all of them.
 FETCH_SCALE = 2.0
 WRITE_SCALE = 1.0
-DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/csrc/bros_device.h",
+DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/csrc/decode_common.h",
+                  "paper_2504_09590_amd/csrc/bros_device.h",
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
@@ -228,7 +229,7 @@ def main():
         achieved = work["decode"]["bytes"] / (dec_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": decode_traffic(batch.name),
-                "kernel": "bros_attn_decode (decode_split_kernel + decode_merge_kernel)",
+                "kernel": "bros_attn_decode (decode_mfma_kernel + decode_mfma_merge_kernel)",
                 "bytes_per_launch": work["decode"]["bytes"], "avg_launch_us": round(dec_ms * 1e3, 2)}
 
     value = work["step_bytes"] / (ms * 1e-3) / 1e9
