@@ -8,14 +8,16 @@
 // Tiling. A workgroup (4 waves) owns one (sequence, KV head, tile of QT
 // positions) and all G = Hq / Hkv query heads of that KV head: 128 query rows,
 // 32 per wave. Keys stream through LDS 64 at a time (four 16-slot blocks, one
-// per wave), double-buffered: the next tile is fetched into registers while
-// the current one is used, then staged into the other buffer. K is staged
-// row-major [key][d] (272-byte rows), V transposed [d][key] (144-byte rows
-// whose 8-byte key groups are XOR-swizzled by d / 8), which makes both the
-// staging writes and the operand reads free of bank conflicts. The logical
-// position of every staged key (or "invalid") sits beside them. Slots past
-// the context or behind an invalid table entry are staged as zeros, so the
-// matrix cores never see whatever the pool holds there.
+// per wave), double-buffered. The pool's K and V rows go straight from global
+// memory into LDS (global_load_lds, no registers, no vector ALU), both
+// row-major [key][d] with the 16-byte chunks of row r permuted by
+// chunk ^ swz(r); the V^T operand is read with the transposing LDS load
+// (ds_read_b64_tr_b16). With that permutation the K operand reads and the
+// transposing V reads are both free of bank conflicts. The logical position
+// of every key (or "invalid") sits beside them. V rows of slots past the
+// context or behind an invalid table entry are overwritten with zeros once
+// their load has landed, so the matrix cores never multiply whatever the
+// pool holds there (K rows there only produce scores that are masked).
 //
 // Both products run transposed, S^T = K Q^T and O^T += V^T P^T, with
 // v_mfma_f32_32x32x16_bf16. In that orientation lane l owns query row l % 32:
@@ -46,8 +48,8 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 
 constexpr int kThreads = 256;
 constexpr int kKeys = 64;                          // keys per LDS tile (4 blocks)
-constexpr int kKRow = kHeadDim * 2 + 16;           // bytes per staged K row (padded)
-constexpr int kVRow = kKeys * 2 + 16;              // bytes per staged V^T row (padded)
+constexpr int kRowBytes = kHeadDim * 2;           // bytes of one K or V row
+constexpr int kTileBytes = kKeys * kRowBytes;      // one K or V tile in LDS
 constexpr int kRowsPerWave = 32;
 constexpr float kRescaleSlack = 8.0f;              // log2 units
 constexpr float kNoMax = -1.0e30f;
@@ -58,14 +60,43 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {   // round 
   const float2_t f = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
-// V^T layout: the 4-key group `chunk` (keys 4*chunk .. +3) of row d sits at
-// byte d * kVRow + 8 * (chunk ^ (d / 8 % 16)).
+// 16-byte chunk c of row r of a K or V tile sits at byte r * 256 + 16 * (c ^ swz(r)).
+__device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_read_tr(const uint8_t* p) {   // ds_read_b64_tr_b16
+  const v4s_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (v4s_t __attribute__((address_space(3)))*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+__device__ __forceinline__ void load_to_lds(const uint16_t* src, uint8_t* dst) {   // 16 bytes per lane at dst + 16 * lane
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                   (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+// Workgroup barrier for the tile pipeline: this wave's LDS reads and writes
+// are complete (lgkmcnt 0) and the compiler may not move memory accesses
+// across it. Loads into LDS still in flight (the tile two ahead) are not
+// waited for -- a fence would wait for them -- so the wave that issued a tile
+// waits for it explicitly (wait_vmem) before the barrier that publishes it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+// s_waitcnt with only the vector-memory count limited (expcnt and lgkmcnt at maximum).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
 
 template <int G>
 __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a) {
   constexpr int QT = 128 / G;   // positions per tile
-  __shared__ __attribute__((aligned(16))) uint8_t s_k[2][kKeys * kKRow];
-  __shared__ __attribute__((aligned(16))) uint8_t s_vt[2][kHeadDim * kVRow];
+  // one array per buffer, so the compiler sees that reads of one buffer do not
+  // alias the loads in flight into the other
+  __shared__ __attribute__((aligned(1024))) uint8_t s_k0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t s_k1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t s_v0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t s_v1[kTileBytes];
   __shared__ __attribute__((aligned(16))) int s_kpos[2][kKeys];
   __shared__ int s_blk_ok[2][4];   // the tile's four table entries were valid
   __shared__ int s_tbl[kMaxTableLds];
@@ -141,18 +172,25 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a
 
   const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
   const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
-  // Staging: wave u copies block u of the tile; lane (sq, dc) copies slots
-  // 4sq .. 4sq+3 and head dims [8dc, 8dc+8) of its K and V tiles.
-  const int sq = lane >> 4;
-  const int dc = lane & 15;
-  // V^T staging: rows 8dc .. 8dc+7, key group (4wv + sq) swizzled by dc
-  const int vt_write_base = 8 * dc * kVRow + ((((4 * wv + sq) ^ dc) & 15) << 3);
-  // V^T operand reads: row d = 32dt + mrow, group 4c2 + 2hi + half; the
-  // swizzle (d/8 = 4dt + mrow/8) splits into a per-lane low part and a
-  // compile-time high part: group ^ swz = 4 (c2 ^ dt) + ((2hi + half) ^ (mrow/8 % 4)).
-  const int swz_lo = (mrow >> 3) & 3;
-  const int vt_read_lo = mrow * kVRow + ((half ^ swz_lo) << 3);
-  const int vt_read_hi = mrow * kVRow + (((2 + half) ^ swz_lo) << 3);
+  // Loads: wave wv brings block wv of the tile, rows 16wv .. 16wv + 15; load i
+  // covers rows 16wv + 4i + lane / 16, lane writing physical chunk lane % 16,
+  // which holds logical chunk (lane % 16) ^ swz(row).
+  const int ld_slot = lane >> 4;
+  // K operand (S^T = K Q^T, d-step c): row 32st + mrow, logical chunk 2c + half.
+  const int k_sw = swz(mrow);
+  const int k_lane = mrow * kRowBytes + (((half ^ k_sw) & 1) << 4);
+  // V^T operand via the transposing read, per (dt, part): lane (group j = lane /
+  // 16, q = lane % 4, t = lane % 16 / 4) reads dims 32dt + 16(j % 2) + 4q ..+3 of
+  // key 16c2 + 8part + 4half + t (key order shared with the P operand).
+  const int tr_j = lane >> 4, tr_q = lane & 3, tr_t = (lane >> 2) & 3;
+  int v_off[2];   // per part, without the dt-dependent chunk bits
+  int v_sw[2];
+#pragma unroll
+  for (int part = 0; part < 2; ++part) {
+    const int key = 8 * part + 4 * half + tr_t;   // mod 16; + 16c2 is a row offset
+    v_sw[part] = swz(key);
+    v_off[part] = key * kRowBytes + ((((2 * (tr_j & 1) + (tr_q >> 1)) ^ v_sw[part]) & 3) << 4) + (tr_q & 1) * 8;
+  }
 
   // The sequence's table entries for this chunk, staged once in LDS, so a
   // table lookup never adds a global load inside the tile loop.
@@ -166,78 +204,49 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a
     return (blk >= 0 && blk < a.num_blocks) ? blk : -1;
   };
 
-  // Two register sets (A, B): tile kt + 2 is requested while tile kt is
-  // computed. Every fetch issues exactly eight loads (an invalid block reads
-  // block 0 and is zeroed when staged), so the waits before staging only
-  // cover the older set.
-  uint4 kA[4], vA[4], kB[4], vB[4];
-  int blkA = -1, blkB = -1;
-  auto fetch = [&](int kt, auto set) __attribute__((always_inline)) {
-    constexpr int SET = decltype(set)::value;
-    uint4(&kr)[4] = SET == 0 ? kA : kB;
-    uint4(&vr)[4] = SET == 0 ? vA : vB;
+  // Tile kt into buffer `buf`: eight 1 KiB loads per wave, always issued (a
+  // tile past the end reads block 0 and is marked invalid), so the wait for the
+  // older tile is an exact count.
+  auto load_tile = [&](int kt, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
+    uint8_t* dk = BUF == 0 ? s_k0 : s_k1;
+    uint8_t* dv = BUF == 0 ? s_v0 : s_v1;
     const int blk = table(kt * 4 + wv);
-    if constexpr (SET == 0) blkA = blk; else blkB = blk;
-    const size_t base = (((size_t)max(blk, 0) * a.num_kv_heads + g) * kBlockSize + 4 * sq) * kHeadDim + 8 * dc;
+    const size_t base = ((size_t)max(blk, 0) * a.num_kv_heads + g) * kBlockSize * kHeadDim;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      kr[j] = *reinterpret_cast<const uint4*>(kpool + base + j * kHeadDim);
-      vr[j] = *reinterpret_cast<const uint4*>(vpool + base + j * kHeadDim);
+    for (int i = 0; i < 4; ++i) {
+      const int row = 16 * wv + 4 * i + ld_slot;
+      const size_t src = base + (size_t)(4 * i + ld_slot) * kHeadDim + (size_t)(((lane & 15) ^ swz(row)) << 3);
+      load_to_lds(kpool + src, dk + (16 * wv + 4 * i) * kRowBytes);
+      load_to_lds(vpool + src, dv + (16 * wv + 4 * i) * kRowBytes);
     }
   };
-  auto stage = [&](int buf, int kt, auto set) __attribute__((always_inline)) {
-    constexpr int SET = decltype(set)::value;
-    uint4(&kr)[4] = SET == 0 ? kA : kB;
-    uint4(&vr)[4] = SET == 0 ? vA : vB;
-    const int blk = SET == 0 ? blkA : blkB;
+  // Once this wave's loads of tile kt have landed: zero the V rows of slots
+  // that are not context, record key positions and block validity.
+  auto fixup = [&](int kt, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
+    uint8_t* dv = BUF == 0 ? s_v0 : s_v1;
     const int b = kt * 4 + wv;
-    const int key0 = 16 * wv + 4 * sq;
-    if (!(blk >= 0 && (b + 1) * kBlockSize <= ctx)) {   // tail or invalid block: zero what is not context
+    const int blk = table(b);
+    if (!(blk >= 0 && (b + 1) * kBlockSize <= ctx)) {   // tail or invalid block
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (!(blk >= 0 && b * kBlockSize + slot_of_offset(4 * sq + j, dirv) < ctx)) {
-          kr[j] = make_uint4(0, 0, 0, 0);
-          vr[j] = kr[j];
-        }
+      for (int p4 = 0; p4 < 4; ++p4) {
+        const int slot = 4 * p4 + ld_slot;
+        if (!(blk >= 0 && b * kBlockSize + slot_of_offset(slot, dirv) < ctx))
+          *reinterpret_cast<uint4*>(dv + (16 * wv + slot) * kRowBytes + (lane & 15) * 16) = make_uint4(0, 0, 0, 0);
       }
     }
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<uint4*>(s_k[buf] + (key0 + j) * kKRow + dc * 16) = kr[j];
-    // V^T: dims 2k and 2k+1 of the four slots, as two 8-byte key groups
-    const uint32_t w0[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-    const uint32_t w1[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
-    const uint32_t w2[4] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w};
-    const uint32_t w3[4] = {vr[3].x, vr[3].y, vr[3].z, vr[3].w};
-    // rows d = 8dc + 2k (+1) all have d / 8 = dc, so the swizzled group is
-    // the same for the eight rows this lane writes
-    uint8_t* vt_lane = s_vt[buf] + vt_write_base;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      uint2 lo, hi;
-      lo.x = __builtin_amdgcn_perm(w1[k], w0[k], 0x05040100u);
-      lo.y = __builtin_amdgcn_perm(w3[k], w2[k], 0x05040100u);
-      hi.x = __builtin_amdgcn_perm(w1[k], w0[k], 0x07060302u);
-      hi.y = __builtin_amdgcn_perm(w3[k], w2[k], 0x07060302u);
-      *reinterpret_cast<uint2*>(vt_lane + (2 * k) * kVRow) = lo;
-      *reinterpret_cast<uint2*>(vt_lane + (2 * k + 1) * kVRow) = hi;
+    if (lane < kBlockSize) {
+      const int pos = b * kBlockSize + slot_of_offset(lane, dirv);
+      s_kpos[BUF][16 * wv + lane] = (blk >= 0 && pos < ctx) ? pos : INT_MAX;
     }
-    if (dc == 0) {
-      int kp[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int pos = b * kBlockSize + slot_of_offset(4 * sq + j, dirv);
-        kp[j] = (blk >= 0 && pos < ctx) ? pos : INT_MAX;
-      }
-      *reinterpret_cast<int4*>(&s_kpos[buf][key0]) = make_int4(kp[0], kp[1], kp[2], kp[3]);
-    }
-    if (lane == 0) s_blk_ok[buf][wv] = blk >= 0;
+    if (lane == 0) s_blk_ok[BUF][wv] = blk >= 0;
   };
 
-  auto compute = [&](int kt) __attribute__((always_inline)) {
-    const int buf = kt & 1;
-    const uint8_t* sk = s_k[buf];
-    const uint8_t* svt = s_vt[buf];
+  auto compute = [&](int kt, auto bufc) __attribute__((always_inline)) {
+    constexpr int buf = decltype(bufc)::value;
+    const uint8_t* sk = buf == 0 ? s_k0 : s_k1;
+    const uint8_t* sv = buf == 0 ? s_v0 : s_v1;
     const int* skpos = s_kpos[buf];
 
     // S^T = K Q^T for keys [32*st, 32*st + 32).
@@ -247,7 +256,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a
       sacc[st] = floatx16{};
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
-        const uint4 kv = *reinterpret_cast<const uint4*>(sk + (32 * st + mrow) * kKRow + (16 * c + 8 * half) * 2);
+        // logical chunk 2c + half of row 32st + mrow (swz(32st + mrow) = swz(mrow))
+        const uint4 kv = *reinterpret_cast<const uint4*>(sk + 32 * st * kRowBytes + k_lane + (((2 * c) ^ (k_sw & 14)) << 4));
         sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[c], sacc[st], 0, 0, 0);
       }
     }
@@ -323,38 +333,44 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a
     // 16c2 + 8 + 4*half + {0..3}, the same permutation the P operand carries.
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
+      // chunk 4dt + (2(j % 2) + q / 2) of the row: the dt bits XOR the swizzle's high bits
+      const int off0 = v_off[0] + (((4 * dt) ^ (v_sw[0] & 12)) << 4);
+      const int off1 = v_off[1] + (((4 * dt) ^ (v_sw[1] & 12)) << 4);
 #pragma unroll
       for (int c2 = 0; c2 < 4; ++c2) {
-        const int cst = 32 * dt * kVRow + 32 * (c2 ^ dt);
-        const uint2 lo = *reinterpret_cast<const uint2*>(svt + vt_read_lo + cst);
-        const uint2 hi = *reinterpret_cast<const uint2*>(svt + vt_read_hi + cst);
+        const uint2 lo = lds_read_tr(sv + 16 * c2 * kRowBytes + off0);
+        const uint2 hi = lds_read_tr(sv + 16 * c2 * kRowBytes + off1);
         const uint4 vv = make_uint4(lo.x, lo.y, hi.x, hi.y);
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pf[c2], o[dt], 0, 0, 0);
       }
     }
   };
 
-  // Tile kt is computed from buffer kt % 2 while tile kt + 1 (already in
-  // registers) is staged into the other buffer, which was last read before
-  // the previous barrier; tile kt + 2 is requested before the computing starts.
-  using SetA = std::integral_constant<int, 0>;
-  using SetB = std::integral_constant<int, 1>;
-  // Fetches and stages run unconditionally (a tile past the end reads block 0
-  // and stages zeros into the buffer nobody reads next), so every iteration
-  // issues the same loads and the waits stay exact; only compute is guarded.
-  fetch(0, SetA{});
-  fetch(1, SetB{});
-  stage(0, 0, SetA{});
-  __syncthreads();
+  // Tile kt is computed from buffer kt % 2 while tile kt + 1 lands in the
+  // other; after the barrier that frees a buffer, the tile two ahead is
+  // requested into it, then this wave waits for its own loads of the next tile
+  // (every older load: eight per tile are younger), fixes it up, and a second
+  // barrier publishes it.
+  using Buf0 = std::integral_constant<int, 0>;
+  using Buf1 = std::integral_constant<int, 1>;
+  load_tile(0, Buf0{});
+  load_tile(1, Buf1{});
+  wait_vmem<8>();
+  fixup(0, Buf0{});
+  lds_barrier();
   for (int kt = 0; kt < n_tiles; kt += 2) {
-    fetch(kt + 2, SetA{});
-    compute(kt);
-    stage(1, kt + 1, SetB{});
-    __syncthreads();
-    fetch(kt + 3, SetB{});
-    if (kt + 1 < n_tiles) compute(kt + 1);
-    stage(0, kt + 2, SetA{});
-    __syncthreads();
+    compute(kt, Buf0{});
+    lds_barrier();
+    load_tile(kt + 2, Buf0{});
+    wait_vmem<8>();
+    fixup(kt + 1, Buf1{});
+    lds_barrier();
+    if (kt + 1 < n_tiles) compute(kt + 1, Buf1{});
+    lds_barrier();
+    load_tile(kt + 3, Buf1{});
+    wait_vmem<8>();
+    fixup(kt + 2, Buf0{});
+    lds_barrier();
   }
 
   // Each half-wave summed its own keys; the row total is their sum.
