@@ -121,3 +121,61 @@ def test_shared_tail_blocks_are_read_per_sequence():
     poison_unowned(b)
     announce("decode over shared RT/BE tail blocks")
     compare(run_decode(b), ref_decode(b), "bf16", "shared tails")
+
+
+def _sample_rows(batch, k=12, seed=0):
+    """The longest and shortest decode rows plus a seeded random sample."""
+    P = batch.num_prefill
+    ctx = batch.ctx_lens[P:]
+    rng = np.random.default_rng(seed)
+    pick = {int(np.argmax(ctx)), int(np.argmin(ctx))}
+    pick.update(int(i) for i in rng.choice(len(ctx), size=min(k, len(ctx)), replace=False))
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("config", [4, 5])
+def test_full_size_workloads_on_sampled_rows(config):
+    # The 70B-shaped (G = 8, ctx up to 16384) and memory-pressure (512 rows,
+    # 100 % occupied pool) workloads in the launch the benchmark times; the
+    # oracle checks a sample of rows one by one.
+    b = W.generate(config)
+    rows = _sample_rows(b, seed=config)
+    announce(f"decode {b.name} S={b.num_seqs} sum_ctx={int(b.ctx_lens.sum())} rows={rows}")
+    got = run_decode(b)
+    compare(got[rows], ref_decode(b, seqs=rows)[rows], "bf16", f"{b.name} sampled rows")
+    assert np.isfinite(oracle.widen(got, "bf16")).all()
+
+
+def test_more_rows_than_the_prefix_holds_in_lds():
+    # Above 4096 rows the per-row tile prefix is kept per chunk of rows.
+    rng = np.random.default_rng(12)
+    n = 4500
+    ctx = rng.integers(1, 49, n)
+    cls = [W.RT if i % 3 == 0 else W.BE for i in range(n)]
+    b = W.custom(ctx, cls, 8, 8, seed=12, spare_blocks=9)
+    poison_unowned(b)
+    announce(f"decode {n} rows, ctx 1..48")
+    compare(run_decode(b), ref_decode(b), "bf16", "4500 rows")
+
+
+def test_workspace_reused_across_batches():
+    # Partials left in a workspace by one call must not leak into the next.
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    a = W.custom([9000, 40, 3000, 17], [W.BE, W.RT, W.BE, W.RT], 32, 8, seed=13)
+    c = W.custom([5000, 2000, 33, 700, 12000], [W.BE, W.BE, W.RT, W.RT, W.BE], 32, 8, seed=14)
+    wsb = max(bros.bros_attn_workspace_size(0, bros.BROS_BF16, x.num_seqs, 32, 128, int(x.ctx_lens.max()))
+              for x in (a, c))
+    ws = torch.full((wsb,), 0x7F, dtype=torch.uint8, device="cuda")   # finite garbage everywhere
+    announce("decode two batches through one workspace")
+    outs = []
+    for x in (a, c, a):
+        dev = bros.to_device(x)
+        out = torch.empty_like(dev.q_decode)
+        bros.bros_attn_decode(out, dev.q_decode, dev.k_pool, dev.v_pool, dev.block_tables, dev.dir, dev.cls,
+                              dev.ctx_lens, int(x.ctx_lens.max()), workspace=ws)
+        torch.cuda.synchronize()
+        outs.append(bros.to_host_bits(out))
+    compare(outs[0], ref_decode(a), "bf16", "first batch")
+    compare(outs[1], ref_decode(c), "bf16", "second batch")
+    assert np.array_equal(outs[0], outs[2])

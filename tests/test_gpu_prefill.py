@@ -102,3 +102,12 @@ def test_last_row_matches_decode_at_the_same_length():
     got = oracle.widen(run_prefill(b), "bf16")[-1]
     ref = oracle.decode(b.q_prefill[-1:], b.k_pool, b.v_pool, b.block_tables[:1], b.dir[:1], b.ctx_lens[:1], "bf16")[0]
     assert np.abs(got - ref).max() <= 2e-2
+
+
+def test_bf16_context_beyond_the_matrix_core_path():
+    # max_ctx above 32768 routes bf16 prefill through the decode kernel in row
+    # mode (every chunk row a decode row with its own causal context).
+    b = written(chunk_batch([33000], [40], [W.RT], group=4, hkv=1, seed=15))
+    poison_unowned(b)
+    announce("prefill bf16 c0=33000 n=40 (row-mode path)")
+    compare(run_prefill(b), ref_prefill(b), "bf16", "bf16 ctx > 32768")
