@@ -3,11 +3,12 @@
 // right end; Sec. 5.1), with the exclusive view of Sec. 5.2 (entry i of a
 // sequence's table holds its positions [16 i, 16 i + 16)).
 //
-// One workgroup moves kTokens tokens. The first lanes resolve each token's
-// destination (sequence by prefix search over cu_new staged in LDS, position,
-// table entry, slot); then all 256 threads copy 16-byte chunks, every load of
-// a thread issued before its first store. Writes are slot-granular, so two
-// sequences sharing a block never race.
+// One workgroup moves kTokens tokens. Its 256 threads first request the
+// tokens' source rows (16-byte chunks), which do not depend on the
+// destination; meanwhile each thread checks one sequence's range of new
+// tokens and resolves the destination (position, table entry, slot) of
+// those that fall in this workgroup; then the chunks are stored. Writes are
+// slot-granular, so two sequences sharing a block never race.
 #include "bros_device.h"
 #include "bros_kernels.h"
 
@@ -16,43 +17,16 @@ namespace {
 
 constexpr int kTokens = 8;          // tokens per workgroup
 constexpr int kThreads = 256;
-constexpr int kMaxSeqLds = 4096;    // prefix array staged in LDS up to this many sequences
 constexpr int kMaxIter = 8;         // 16-byte chunks per thread per pass
+
+typedef unsigned v4u_t __attribute__((ext_vector_type(4)));   // 16 bytes (a plain vector promotes to registers)
 
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
-  __shared__ int s_cu[kMaxSeqLds + 1];
   __shared__ int s_dst[kTokens];   // block * 16 + slot, or -1 when the token is skipped
 
   const int tid = threadIdx.x;
   const int t0 = blockIdx.x * kTokens;
-  const bool staged = a.num_seqs <= kMaxSeqLds;
-  if (staged) {
-    for (int i = tid; i <= a.num_seqs; i += kThreads) s_cu[i] = a.cu_new[i];
-  }
-  __syncthreads();
-
-  if (tid < kTokens) {
-    const int t = t0 + tid;
-    int dst = -1;
-    if (t < a.num_new_tokens) {
-      int s = staged ? upper_index(s_cu, a.num_seqs + 1, t)
-                     : upper_index(a.cu_new, a.num_seqs + 1, t);
-      s = min(s, a.num_seqs - 1);   // a token past cu_new[num_seqs] stays in bounds
-      const int first = staged ? s_cu[s] : a.cu_new[s];
-      const int p = a.pos0[s] + (t - first);
-      if (p >= 0) {
-        const int bi = p >> 4;
-        if (bi < a.max_blocks_per_seq) {
-          const int blk = a.block_tables[(size_t)s * a.max_blocks_per_seq + bi];
-          if (blk >= 0 && blk < a.num_blocks)
-            dst = blk * kBlockSize + slot_of_offset(p & 15, seq_direction(a.dir, a.cls, s));
-        }
-      }
-    }
-    s_dst[tid] = dst;
-  }
-  __syncthreads();
 
   constexpr int kElem = BF16 ? 2 : 4;
   constexpr int kChunksPerRow = kHeadDim * kElem / 16;     // 16-byte chunks per head row
@@ -64,40 +38,83 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
   uint8_t* __restrict__ vpool = static_cast<uint8_t*>(a.v_pool);
   const size_t row_bytes = (size_t)kHeadDim * kElem;
 
-  for (int base = 0; base < total; base += kThreads * kMaxIter) {
-    uint4 data[kMaxIter];
-    size_t dst_off[kMaxIter];
-    bool live[kMaxIter];
-    bool is_v[kMaxIter];
+  // Chunk idx of the workgroup: token, tensor (0 = K, 1 = V), chunk within the token.
+#define BROS_KVW_SPLIT(idx)                                  \
+  const int tok = (idx) / (2 * chunks_per_token);            \
+  const int rem = (idx) - tok * 2 * chunks_per_token;        \
+  const int tensor = rem / chunks_per_token;                 \
+  const int c = rem - tensor * chunks_per_token;
+
+  // Source rows of the first pass: they do not depend on where the tokens go,
+  // so they are requested before the destinations are resolved.
+  v4u_t data[kMaxIter];
+#pragma unroll
+  for (int it = 0; it < kMaxIter; ++it) {
+    const int idx = it * kThreads + tid;
+    if (idx < total) {
+      BROS_KVW_SPLIT(idx)
+      if (t0 + tok < a.num_new_tokens)
+        data[it] = *reinterpret_cast<const v4u_t*>((tensor ? vnew : knew) + ((size_t)(t0 + tok) * chunks_per_token + c) * 16);
+    }
+  }
+
+  // Destinations: thread j checks whether sequence j holds any of this
+  // workgroup's tokens (one round of loads: its prefix offsets, first position
+  // and direction), and resolves those tokens' table entries (a second round).
+  // A token in no sequence's range is skipped.
+  if (tid < kTokens) s_dst[tid] = -1;
+  __syncthreads();
+  for (int j = tid; j < a.num_seqs; j += kThreads) {
+    const int lo = a.cu_new[j], hi = a.cu_new[j + 1];
+    const int p0 = a.pos0[j];
+    const int dirv = seq_direction(a.dir, a.cls, j);
+    const int k0 = max(lo, t0), k1 = min(hi, min(t0 + kTokens, a.num_new_tokens));
+    for (int k = k0; k < k1; ++k) {
+      const int p = p0 + (k - lo);
+      int dst = -1;
+      if (p >= 0 && (p >> 4) < a.max_blocks_per_seq) {
+        const int blk = a.block_tables[(size_t)j * a.max_blocks_per_seq + (p >> 4)];
+        if (blk >= 0 && blk < a.num_blocks) dst = blk * kBlockSize + slot_of_offset(p & 15, dirv);
+      }
+      s_dst[k - t0] = dst;
+    }
+  }
+  __syncthreads();
+
+  // Store one pass's chunks to their slots.
+#define BROS_KVW_STORE(base, arr)                                                                   \
+  _Pragma("unroll") for (int it = 0; it < kMaxIter; ++it) {                                         \
+    const int idx = (base) + it * kThreads + tid;                                                   \
+    if (idx < total) {                                                                              \
+      BROS_KVW_SPLIT(idx)                                                                           \
+      const int h = c / kChunksPerRow;                                                              \
+      const int cc = c - h * kChunksPerRow;                                                         \
+      const int dst = s_dst[tok];                                                                   \
+      if (dst >= 0 && t0 + tok < a.num_new_tokens) {                                                \
+        const int blk = dst >> 4, slot = dst & 15;                                                  \
+        const size_t off = (((size_t)blk * a.num_kv_heads + h) * kBlockSize + slot) * row_bytes +   \
+                           (size_t)cc * 16;                                                         \
+        *reinterpret_cast<v4u_t*>((tensor ? vpool : kpool) + off) = arr[it];                        \
+      }                                                                                             \
+    }                                                                                               \
+  }
+  BROS_KVW_STORE(0, data)
+  // Further passes (more than eight KV heads): load, then store.
+  for (int base = kThreads * kMaxIter; base < total; base += kThreads * kMaxIter) {
+    v4u_t more[kMaxIter];
 #pragma unroll
     for (int it = 0; it < kMaxIter; ++it) {
       const int idx = base + it * kThreads + tid;
-      live[it] = false;
-      is_v[it] = false;
-      dst_off[it] = 0;
       if (idx < total) {
-        const int tok = idx / (2 * chunks_per_token);
-        const int rem = idx - tok * 2 * chunks_per_token;
-        const int tensor = rem / chunks_per_token;          // 0 = K, 1 = V
-        const int c = rem - tensor * chunks_per_token;
-        const int h = c / kChunksPerRow;
-        const int cc = c - h * kChunksPerRow;
-        const int dst = s_dst[tok];
-        if (dst >= 0 && t0 + tok < a.num_new_tokens) {
-          const size_t src_off = ((size_t)(t0 + tok) * a.num_kv_heads + h) * row_bytes + (size_t)cc * 16;
-          data[it] = *reinterpret_cast<const uint4*>((tensor ? vnew : knew) + src_off);
-          const int blk = dst >> 4, slot = dst & 15;
-          dst_off[it] = (((size_t)blk * a.num_kv_heads + h) * kBlockSize + slot) * row_bytes + (size_t)cc * 16;
-          live[it] = true;
-          is_v[it] = tensor != 0;
-        }
+        BROS_KVW_SPLIT(idx)
+        if (t0 + tok < a.num_new_tokens)
+          more[it] = *reinterpret_cast<const v4u_t*>((tensor ? vnew : knew) + ((size_t)(t0 + tok) * chunks_per_token + c) * 16);
       }
     }
-#pragma unroll
-    for (int it = 0; it < kMaxIter; ++it) {
-      if (live[it]) *reinterpret_cast<uint4*>((is_v[it] ? vpool : kpool) + dst_off[it]) = data[it];
-    }
+    BROS_KVW_STORE(base, more)
   }
+#undef BROS_KVW_STORE
+#undef BROS_KVW_SPLIT
 }
 
 }  // namespace
