@@ -5,31 +5,41 @@
 // sequence s sits at position c0 + j, c0 = ctx - n, and attends to positions
 // 0 .. c0 + j of the sequence, gathered from the bidirectional pool (Sec. 5.1).
 //
-// Tiling. A workgroup (4 waves) owns one (sequence, KV head, tile of QT
-// positions) and all G = Hq / Hkv query heads of that KV head: 128 query rows,
-// 32 per wave. Keys stream through LDS 64 at a time (four 16-slot blocks, one
-// per wave), double-buffered. The pool's K and V rows go straight from global
-// memory into LDS (global_load_lds, no registers, no vector ALU), both
-// row-major [key][d] with the 16-byte chunks of row r permuted by
-// chunk ^ swz(r); the V^T operand is read with the transposing LDS load
-// (ds_read_b64_tr_b16). With that permutation the K operand reads and the
-// transposing V reads are both free of bank conflicts. The logical position
-// of every key (or "invalid") sits beside them. V rows of slots past the
-// context or behind an invalid table entry are overwritten with zeros once
-// their load has landed, so the matrix cores never multiply whatever the
-// pool holds there (K rows there only produce scores that are masked).
+// Work units. A workgroup (8 waves, two per SIMD) owns one (sequence, KV
+// head, tile of 128 / G positions): 128 query rows, all G = Hq / Hkv query
+// heads of that KV head. Waves 0-3 take rows 0-31, 32-63, 64-95, 96-127 over
+// the even 32-key tiles of the context, waves 4-7 the same rows over the odd
+// tiles, so a unit's chain is half its key tiles long; the two halves are
+// merged through LDS at the end. Two waves per SIMD let one wave's vector
+// work (the softmax) run beside the other's matrix-core products: a single
+// wave issues vector instructions at about half the rate two waves reach.
+// Workgroups are launched longest unit first (ranked on the device from the
+// length table), and consecutive ids are spread over the XCDs so that one KV
+// head of every sequence stays on one XCD's L2.
 //
-// Both products run transposed, S^T = K Q^T and O^T += V^T P^T, with
-// v_mfma_f32_32x32x16_bf16. In that orientation lane l owns query row l % 32:
-// its 16 accumulator values of S^T are 16 keys of its own row, so the row
-// max / sum need only one exchange between the two half-waves, the O rescale
-// is lane-local, and the P operand of the second product is read straight out
-// of the S accumulator (keys are permuted identically in P and V^T; the sum
-// over keys does not care). The causal mask compares each key's logical
-// position with the row's position, only on tiles that reach the diagonal or
-// the context end: direction only reorders keys inside a block, which neither
-// product sees. The running max moves lazily (only when a score exceeds it by
-// more than 2^8), so the O rescale is rare.
+// Data path. K and V rows go straight from the pool into LDS
+// (global_load_lds, no registers), row-major [key][d] with the 16-byte chunks
+// of row r permuted by chunk ^ swz(r), which makes both the K operand reads
+// and the transposing V^T reads (ds_read_b64_tr_b16) free of bank conflicts.
+// K and V have rings of their own (four slots each): the K tile of step i + 1
+// is read while the V tile of step i is, and each slot is refilled four steps
+// ahead of its use. Table entries arrive as scalar loads a step ahead.
+//
+// Software pipeline (per wave, per step): the scores S^T = K Q^T of the next
+// tile are computed on the matrix cores while the vector ALU turns the current
+// tile's scores into probabilities, then O^T += V^T P^T; the max of the next
+// tile's scores decides the rescale before the step ends. In the transposed
+// orientation lane l owns query row l % 32, so the row max and sum need one
+// exchange between the two half-waves, the O rescale is lane-local, and the P
+// operand is built straight from the score accumulators (keys are permuted
+// identically in P and V^T; the sum over keys does not care). The causal
+// mask compares each key's logical position with the row's position, only on
+// tiles that reach the diagonal, the context end or an invalid table entry:
+// direction only reorders keys inside a block, which neither product sees.
+// V rows of slots that are not context are zeroed in LDS, so the matrix
+// cores never multiply whatever the pool holds there. The running max moves
+// lazily (only when a score exceeds it by more than 2^8), so the O rescale
+// is rare.
 #include "bros_device.h"
 #include "bros_kernels.h"
 
@@ -45,17 +55,21 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
 typedef __attribute__((__vector_size__(2 * sizeof(float)))) float float2_t;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
+typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
+typedef short v4s_t __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
-constexpr int kKeys = 64;                          // keys per LDS tile (4 blocks)
-constexpr int kRowBytes = kHeadDim * 2;           // bytes of one K or V row
+constexpr int kThreads = 512;                       // 8 waves: two per SIMD
+constexpr int kRows = 128;                         // query rows per workgroup
+constexpr int kKeys = 32;                          // keys per tile (2 blocks)
+constexpr int kSlots = 4;                          // stages of the K ring and of the V ring
+constexpr int kRowBytes = kHeadDim * 2;            // bytes of one K or V row
 constexpr int kTileBytes = kKeys * kRowBytes;      // one K or V tile in LDS
-constexpr int kRowsPerWave = 32;
 constexpr float kRescaleSlack = 8.0f;              // log2 units
 constexpr float kNoMax = -1.0e30f;
-constexpr int kMaxTableLds = kPrefillMaxCtxMfma / kBlockSize;   // table entries staged in LDS
+constexpr int kMaxRankItems = kThreads;            // units ranked by length on the device
+constexpr int kLoadsPerStep = 4;                   // two K and two V loads per wave per step
 
-__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+__device__ __forceinline__ bf16x8_t as_bf16x8(v4u_t v) { return __builtin_bit_cast(bf16x8_t, v); }
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {   // round to nearest even
   const float2_t f = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
@@ -63,330 +77,546 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {   // round 
 // 16-byte chunk c of row r of a K or V tile sits at byte r * 256 + 16 * (c ^ swz(r)).
 __device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
 
-typedef short v4s_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint2 lds_read_tr(const uint8_t* p) {   // ds_read_b64_tr_b16
   const v4s_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (v4s_t __attribute__((address_space(3)))*)(p));
   return __builtin_bit_cast(uint2, v);
 }
-__device__ __forceinline__ void load_to_lds(const uint16_t* src, uint8_t* dst) {   // 16 bytes per lane at dst + 16 * lane
-  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                   (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+// 16 bytes per lane from `src` straight into LDS at dst + 16 * lane
+// (global_load_lds_dwordx4; dst is wave-uniform, passed in M0). Issued as
+// inline assembly so the compiler's own wait insertion neither sees these
+// writes to LDS nor orders LDS reads of other ring slots behind them: the
+// kernel's explicit waits (wait_vmem) and barriers order every access.
+// The source is a wave-uniform base (scalar registers) plus a per-lane byte
+// offset.
+__device__ __forceinline__ void load_to_lds(const void* base, uint32_t lane_off, const uint8_t* dst) {
+  // the LDS aperture is 4 GiB aligned: the low half of a generic pointer into
+  // LDS is the LDS address
+  const uint32_t m0 = (uint32_t)(uintptr_t)dst;
+  asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(lane_off), "s"(base), "{m0}"(__builtin_amdgcn_readfirstlane(m0)));
+}
+// A load the compiler may issue as a scalar (uniform) load.
+typedef const int32_t __attribute__((address_space(4)))* scalar_i32_ptr;
+__device__ __forceinline__ int32_t load_uniform(const int32_t* p, size_t i) {
+  return ((scalar_i32_ptr)p)[i];   // address-space cast: C-style only
 }
 // Workgroup barrier for the tile pipeline: this wave's LDS reads and writes
 // are complete (lgkmcnt 0) and the compiler may not move memory accesses
-// across it. Loads into LDS still in flight (the tile two ahead) are not
-// waited for -- a fence would wait for them -- so the wave that issued a tile
-// waits for it explicitly (wait_vmem) before the barrier that publishes it.
+// across it. Loads into LDS still in flight are not waited for here; each
+// wave waits for its own loads (wait_vmem) before the barrier that publishes
+// them.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
-// s_waitcnt with only the vector-memory count limited (expcnt and lgkmcnt at maximum).
+// Wait until at most N of this wave's vector-memory operations are
+// outstanding (they complete in order); a compiler barrier for memory.
 template <int N>
 __device__ __forceinline__ void wait_vmem() {
-  static_assert(N >= 0 && N < 16, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Maximum of x over lanes l and l ^ 32 (v_permlane32_swap).
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int N>
+using Int = std::integral_constant<int, N>;
+
+// Key tiles of unit (s, t): the keys its last row sees, in tiles of kKeys; 0
+// for a tile past the sequence's rows or inconsistent lengths.
+__device__ __forceinline__ int unit_tiles(const PrefillArgs& a, int s, int t, int qt) {
+  const int q_begin = a.cu_q[s];
+  const int n = a.cu_q[s + 1] - q_begin;
+  const int t0 = t * qt;
+  if (q_begin < 0 || n <= 0 || q_begin + n > a.num_q_tokens || t0 >= n) return 0;
+  const int c0 = a.ctx_lens[s] - n;
+  if (c0 < 0) return 0;
+  const int ctx = min(a.ctx_lens[s], min(a.max_ctx, a.max_blocks_per_seq * kBlockSize));
+  const int kend = min(ctx, c0 + min(n, t0 + qt));
+  return (kend + kKeys - 1) / kKeys;
 }
 
 template <int G>
-__global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a) {
-  constexpr int QT = 128 / G;   // positions per tile
-  // one array per buffer, so the compiler sees that reads of one buffer do not
-  // alias the loads in flight into the other
-  __shared__ __attribute__((aligned(1024))) uint8_t s_k0[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t s_k1[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t s_v0[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t s_v1[kTileBytes];
-  __shared__ __attribute__((aligned(16))) int s_kpos[2][kKeys];
-  __shared__ int s_blk_ok[2][4];   // the tile's four table entries were valid
-  __shared__ int s_tbl[kMaxTableLds];
-
-  // Work order. Consecutive workgroup ids land on different XCDs (id % 8),
-  // each XCD with its own L2. When the number of (sequence, KV head) pairs is
-  // a multiple of 8, pair p takes ids p, p + P, p + 2P, ... (P pairs), so all
-  // its tiles run on XCD p % 8 and share that L2 for their K/V tiles, and
-  // every XCD gets one pair of each group of 8 -- for the usual 8 KV heads,
-  // one KV head of every sequence, which keeps the XCDs evenly loaded however
-  // long the sequences are. Within a pair the longest rows come first.
-  const int L = blockIdx.x;
-  const int P = a.num_seqs * a.num_kv_heads;
-  int pair, tile_rev;
-  if ((P & 7) == 0) {
-    pair = L % P;
-    tile_rev = L / P;
-  } else {
-    pair = L / a.tiles_per_seq;
-    tile_rev = L % a.tiles_per_seq;
-  }
-  const int g = pair % a.num_kv_heads;
-  const int s = pair / a.num_kv_heads;
-  const int tile = a.tiles_per_seq - 1 - tile_rev;
-
-  const int q_begin = a.cu_q[s];
-  const int n = a.cu_q[s + 1] - q_begin;
-  const int t0 = tile * QT;
-  if (q_begin < 0 || n <= 0 || q_begin + n > a.num_q_tokens || t0 >= n) return;
-  const int c0 = a.ctx_lens[s] - n;
-  if (c0 < 0) return;   // inconsistent lengths: rows left untouched
-  const int ctx = min(a.ctx_lens[s], min(a.max_ctx, a.max_blocks_per_seq * kBlockSize));
-  const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
-  const int dirv = seq_direction(a.dir, a.cls, s);
-  const int rows_here = min(n, t0 + QT);
-  const int kend = min(ctx, c0 + rows_here);
-  const int n_tiles = (kend + kKeys - 1) / kKeys;
-  // keys below this logical position are visible to every row of the workgroup
-  const int full_below = min(ctx, c0 + t0 + 1);
+__global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a) {
+  constexpr int QT = kRows / G;   // positions per unit
+  // K ring and V ring, kSlots slots each; a slot holds the even-tile half and
+  // the odd-tile half (kTileBytes each). Slot offsets are compile-time
+  // constants below 64 KiB, so they fold into the LDS instructions' offset
+  // field.
+  constexpr int kSlotBytes = 2 * kTileBytes;
+  __shared__ __attribute__((aligned(1024))) uint8_t s_kring[kSlots * kSlotBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t s_vring[kSlots * kSlotBytes];
+  __shared__ int s_first_bad;
+  __shared__ __attribute__((aligned(16))) int s_len[kMaxRankItems];
+  __shared__ int s_item;
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wv = wave_id_uniform();
+  const int rg = wv & 3;    // row group: rows 32 rg .. 32 rg + 31
+  const int kh = wv >> 2;   // key half: tiles kh, kh + 2, kh + 4, ...
+
+  // ---- Which unit: rank by key tiles, longest first (ties by index). Ids
+  // r * Hkv + g give every rank all KV heads on consecutive ids, i.e. on
+  // different XCDs (id % 8), and one KV head of every unit on one XCD when
+  // Hkv is a multiple of 8.
+  const int Hkv = a.num_kv_heads;
+  const int tps = a.tiles_per_seq;
+  const int n_items = a.num_seqs * tps;
+  const int g = blockIdx.x % Hkv;
+  const int rank = blockIdx.x / Hkv;
+  int item;
+  if (n_items <= kMaxRankItems) {
+    int my_len = -1;   // the padding entries never outrank a unit
+    if (tid < n_items) my_len = unit_tiles(a, tid / tps, tid % tps, QT);
+    s_len[tid] = my_len;
+    __syncthreads();
+    if (tid < n_items) {
+      int r = 0;
+      const int n4 = (n_items + 3) / 4;
+      int j4 = 0;
+      for (; j4 + 4 <= n4; j4 += 4) {   // four reads in flight
+        int4 l4[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) l4[u] = reinterpret_cast<const int4*>(s_len)[j4 + u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int lj[4] = {l4[u].x, l4[u].y, l4[u].z, l4[u].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) r += (lj[e] > my_len) | ((lj[e] == my_len) & (4 * (j4 + u) + e < tid));
+        }
+      }
+      for (; j4 < n4; ++j4) {
+        const int4 l4 = reinterpret_cast<const int4*>(s_len)[j4];
+        const int lj[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r += (lj[e] > my_len) | ((lj[e] == my_len) & (4 * j4 + e < tid));
+      }
+      if (r == rank) s_item = tid;
+    }
+    __syncthreads();
+    item = __builtin_amdgcn_readfirstlane(s_item);
+  } else {
+    // longest tile of every sequence first
+    item = (rank % a.num_seqs) * tps + (tps - 1 - rank / a.num_seqs);
+  }
+  const int s = item / tps;
+  const int t = item % tps;
+
+  // The unit's lengths, as scalar loads.
+  const int q_begin = load_uniform(a.cu_q, s);
+  const int n = load_uniform(a.cu_q, s + 1) - q_begin;
+  const int ctx_s = load_uniform(a.ctx_lens, s);
+  const int t0 = t * QT;
+  if (q_begin < 0 || n <= 0 || q_begin + n > a.num_q_tokens || t0 >= n || ctx_s < n) return;
+  const int c0 = ctx_s - n;
+  const int ctx = min(ctx_s, min(a.max_ctx, a.max_blocks_per_seq * kBlockSize));
+  const int kend = min(ctx, c0 + min(n, t0 + QT));
+  const int n_kt = (kend + kKeys - 1) / kKeys;   // key tiles of the unit
+  if (n_kt == 0) return;
+  const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
+  const int dirv = seq_direction(a.dir, a.cls, s);
+  // keys below this logical position are visible to every row of the unit
+  const int full_below = min(ctx, c0 + t0 + 1);
+  const int n_steps = (n_kt + 1) / 2;        // both halves step together
+  const int n_mine = (n_kt - kh + 1) / 2;     // tiles of this wave's half
+
   const int half = lane >> 5;
   const int mrow = lane & 31;
-  const int r = kRowsPerWave * wv + mrow;
-  const int head = g * G + r / QT;
-  const int qrow = t0 + r % QT;
+  const int Hq = a.num_q_heads;
+  const int r_unit = 32 * rg + mrow;            // the lane's row in the unit
+  const int head = g * G + r_unit / QT;
+  const int qrow = t0 + r_unit % QT;
   const bool row_valid = qrow < n;
   const int qpos = row_valid ? c0 + qrow : -1;
-  const int Hq = a.num_q_heads;
+  const size_t row_off = ((size_t)(q_begin + min(qrow, n - 1)) * Hq + head) * kHeadDim;   // q / out row
 
-  // Q^T operand: for d-step c, lane holds Q[row][16c + 8*half .. +8).
+  // Q^T operand: for d-step c, lane holds Q[row][16c + 8*half .. +8). Issued
+  // before every load into LDS, so waiting for the first tiles covers it.
   bf16x8_t qf[8];
   {
-    const uint16_t* qp = static_cast<const uint16_t*>(a.q) + ((size_t)(q_begin + qrow) * Hq + head) * kHeadDim;
+    const uint16_t* qp = static_cast<const uint16_t*>(a.q) + row_off;
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (row_valid) v = *reinterpret_cast<const uint4*>(qp + 16 * c + 8 * half);
+      v4u_t v = {0, 0, 0, 0};
+      if (row_valid) v = *reinterpret_cast<const v4u_t*>(qp + 16 * c + 8 * half);
       qf[c] = as_bf16x8(v);
     }
-    // Consume the Q loads here: otherwise the first use inside the tile loop
-    // waits for every outstanding load, including the prefetched tiles.
-#pragma unroll
-    for (int c = 0; c < 8; ++c) asm volatile("" : "+v"(qf[c]));
   }
 
-  floatx16 o[4];
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) o[dt] = floatx16{};
-  float m_run = kNoMax, l_run = 0.0f;
-
+  // Table entries come in as scalar loads (block b of the sequence, or -1
+  // for an entry past the context or out of range). The tile of step j for
+  // this wave's half is 2 j + kh; this wave loads, positions and fixes up
+  // rows 8 rg .. 8 rg + 7 of it, in block rg / 2.
   const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
   const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
-  // Loads: wave wv brings block wv of the tile, rows 16wv .. 16wv + 15; load i
-  // covers rows 16wv + 4i + lane / 16, lane writing physical chunk lane % 16,
-  // which holds logical chunk (lane % 16) ^ swz(row).
+  const int32_t* tbl = a.block_tables + (size_t)s * a.max_blocks_per_seq;
+  auto entry = [&](int b) -> int {
+    const int v = load_uniform(tbl, min(b, nblk - 1));
+    return (b < nblk && v >= 0 && v < a.num_blocks) ? v : -1;
+  };
+  const int my_bt = rg >> 1;                // block of the tile holding this wave's rows
+  const int my_slot0 = 8 * (rg & 1);        // first of its slots
+  auto own = [&](int j) -> int { return entry(2 * (2 * j + kh) + my_bt); };
+
+  // Loads: load i (0, 1) covers tile rows 8 rg + 4i + lane / 16, lane writing
+  // physical chunk lane % 16, which holds logical chunk (lane % 16) ^ swz(row).
+  // A tile past the end (or an invalid entry) loads pool block 0 into a slot
+  // nobody reads, so every step issues exactly kLoadsPerStep loads and the
+  // waits below can count.
   const int ld_slot = lane >> 4;
-  // K operand (S^T = K Q^T, d-step c): row 32st + mrow, logical chunk 2c + half.
+  uint32_t ld_off[2];   // byte offset of the lane's 16 bytes within the block
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = 8 * rg + 4 * i + ld_slot;   // tile row
+    ld_off[i] = (uint32_t)(((my_slot0 + 4 * i + ld_slot) * kHeadDim + (((lane & 15) ^ swz(row)) << 3)) * 2);
+  }
+  auto issue = [&](int j, int blk, const uint16_t* pool, uint8_t* ring) __attribute__((always_inline)) {
+    const int b = (2 * j + kh < n_kt && blk >= 0) ? blk : 0;
+    const uint16_t* base = pool + ((size_t)b * Hkv + g) * kBlockSize * kHeadDim;
+    uint8_t* dst = ring + kh * kTileBytes + 8 * rg * kRowBytes;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) load_to_lds(base, ld_off[i], dst + 4 * i * kRowBytes);
+  };
+  // Once this wave's V loads of step j have landed: zero its rows whose slot
+  // is not context.
+  auto fixup_v = [&](int j, int blk, uint8_t* ring) __attribute__((always_inline)) {
+    const int tile = 2 * j + kh;
+    if (tile >= n_kt) return;
+    const int b = 2 * tile + my_bt;
+    if (blk >= 0 && (b + 1) * kBlockSize <= ctx) return;
+    uint8_t* dv = ring + kh * kTileBytes + 8 * rg * kRowBytes;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int r8 = 4 * p + ld_slot;   // row among the wave's 8
+      if (!(blk >= 0 && b * kBlockSize + slot_of_offset(my_slot0 + r8, dirv) < ctx))
+        *reinterpret_cast<v4u_t*>(dv + r8 * kRowBytes + (lane & 15) * 16) = v4u_t{0, 0, 0, 0};
+    }
+  };
+
+  // K operand (S^T = K Q^T, d-step c): tile row mrow, logical chunk 2c + half.
   const int k_sw = swz(mrow);
   const int k_lane = mrow * kRowBytes + (((half ^ k_sw) & 1) << 4);
   // V^T operand via the transposing read, per (dt, part): lane (group j = lane /
   // 16, q = lane % 4, t = lane % 16 / 4) reads dims 32dt + 16(j % 2) + 4q ..+3 of
   // key 16c2 + 8part + 4half + t (key order shared with the P operand).
   const int tr_j = lane >> 4, tr_q = lane & 3, tr_t = (lane >> 2) & 3;
-  int v_off[2];   // per part, without the dt-dependent chunk bits
+  int v_off[2];
   int v_sw[2];
 #pragma unroll
   for (int part = 0; part < 2; ++part) {
-    const int key = 8 * part + 4 * half + tr_t;   // mod 16; + 16c2 is a row offset
+    const int key = 8 * part + 4 * half + tr_t;
     v_sw[part] = swz(key);
     v_off[part] = key * kRowBytes + ((((2 * (tr_j & 1) + (tr_q >> 1)) ^ v_sw[part]) & 3) << 4) + (tr_q & 1) * 8;
   }
 
-  // The sequence's table entries for this chunk, staged once in LDS, so a
-  // table lookup never adds a global load inside the tile loop.
-  // (The host sends contexts longer than kMaxTableLds blocks to the vector
-  // path, so the whole table of the sequence fits.)
-  const int nblk_tbl = min(nblk, kMaxTableLds);
-  for (int i = tid; i < nblk_tbl; i += kThreads) s_tbl[i] = a.block_tables[(size_t)s * a.max_blocks_per_seq + i];
-  __syncthreads();
-  auto table = [&](int b) -> int {
-    const int blk = b < nblk_tbl ? s_tbl[b] : -1;
-    return (blk >= 0 && blk < a.num_blocks) ? blk : -1;
+  floatx16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o[dt] = floatx16{};
+  float m_run = kNoMax, l_run = 0.0f, alpha = 1.0f;
+  // Raw scores of the wave's next tile in vector registers: read out of the
+  // accumulators once (by the max) and carried to the step that turns them
+  // into probabilities.
+  floatx16 cur;
+  const float sl2 = a.scale_log2;
+
+  // K operands of the tile in K ring `sk` (this wave's half), all eight
+  // d-steps, issued together.
+  auto k_operands = [&](const uint8_t* sk, v4u_t (&kv)[8]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) kv[c] = *reinterpret_cast<const v4u_t*>(sk + k_lane + (((2 * c) ^ (k_sw & 14)) << 4));
   };
-
-  // Tile kt into buffer `buf`: eight 1 KiB loads per wave, always issued (a
-  // tile past the end reads block 0 and is marked invalid), so the wait for the
-  // older tile is an exact count.
-  auto load_tile = [&](int kt, auto bufc) __attribute__((always_inline)) {
-    constexpr int BUF = decltype(bufc)::value;
-    uint8_t* dk = BUF == 0 ? s_k0 : s_k1;
-    uint8_t* dv = BUF == 0 ? s_v0 : s_v1;
-    const int blk = table(kt * 4 + wv);
-    const size_t base = ((size_t)max(blk, 0) * a.num_kv_heads + g) * kBlockSize * kHeadDim;
+  // S^T = K Q^T (one dependent chain; back-to-back accumulation needs no gap).
+  auto scores = [&](const v4u_t (&kv)[8], floatx16& acc) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = 16 * wv + 4 * i + ld_slot;
-      const size_t src = base + (size_t)(4 * i + ld_slot) * kHeadDim + (size_t)(((lane & 15) ^ swz(row)) << 3);
-      load_to_lds(kpool + src, dk + (16 * wv + 4 * i) * kRowBytes);
-      load_to_lds(vpool + src, dv + (16 * wv + 4 * i) * kRowBytes);
-    }
+    for (int c = 0; c < 8; ++c)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[c]), qf[c], c == 0 ? floatx16{} : acc, 0, 0, 0);
   };
-  // Once this wave's loads of tile kt have landed: zero the V rows of slots
-  // that are not context, record key positions and block validity.
-  auto fixup = [&](int kt, auto bufc) __attribute__((always_inline)) {
-    constexpr int BUF = decltype(bufc)::value;
-    uint8_t* dv = BUF == 0 ? s_v0 : s_v1;
-    const int b = kt * 4 + wv;
-    const int blk = table(b);
-    if (!(blk >= 0 && (b + 1) * kBlockSize <= ctx)) {   // tail or invalid block
+  // Move the accumulators to `cur`, mask them (when asked: `tile` is the
+  // tile they belong to) and fold the tile's max into the running max; sets
+  // alpha, the factor O and l take for the new max. Accumulator j is key
+  // k = 8*(j/4) + 4*half + j%4 of the tile: physical slot k % 16 of the
+  // tile's block k / 16, which holds that block's position offset
+  // slot_of_offset(k % 16, dir).
+  auto mask_max = [&](floatx16& acc, auto maskc, int tile) __attribute__((always_inline)) {
 #pragma unroll
-      for (int p4 = 0; p4 < 4; ++p4) {
-        const int slot = 4 * p4 + ld_slot;
-        if (!(blk >= 0 && b * kBlockSize + slot_of_offset(slot, dirv) < ctx))
-          *reinterpret_cast<uint4*>(dv + (16 * wv + slot) * kRowBytes + (lane & 15) * 16) = make_uint4(0, 0, 0, 0);
-      }
+    for (int j = 0; j < 16; ++j) {
+      float v = acc[j];
+      asm volatile("" : "+v"(v));
+      cur[j] = v;
     }
-    if (lane < kBlockSize) {
-      const int pos = b * kBlockSize + slot_of_offset(lane, dirv);
-      s_kpos[BUF][16 * wv + lane] = (blk >= 0 && pos < ctx) ? pos : INT_MAX;
-    }
-    if (lane == 0) s_blk_ok[BUF][wv] = blk >= 0;
-  };
-
-  auto compute = [&](int kt, auto bufc) __attribute__((always_inline)) {
-    constexpr int buf = decltype(bufc)::value;
-    const uint8_t* sk = buf == 0 ? s_k0 : s_k1;
-    const uint8_t* sv = buf == 0 ? s_v0 : s_v1;
-    const int* skpos = s_kpos[buf];
-
-    // S^T = K Q^T for keys [32*st, 32*st + 32).
-    floatx16 sacc[2];
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      sacc[st] = floatx16{};
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        // logical chunk 2c + half of row 32st + mrow (swz(32st + mrow) = swz(mrow))
-        const uint4 kv = *reinterpret_cast<const uint4*>(sk + 32 * st * kRowBytes + k_lane + (((2 * c) ^ (k_sw & 14)) << 4));
-        sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[c], sacc[st], 0, 0, 0);
-      }
-    }
-
-    // Scale to log2 units; mask by logical position where the tile needs it.
-    // Accumulator j of sub-tile st is key 32*st + 8*(j/4) + 4*half + j%4.
-    const bool full = (kt + 1) * kKeys <= full_below && s_blk_ok[buf][0] && s_blk_ok[buf][1] &&
-                      s_blk_ok[buf][2] && s_blk_ok[buf][3];
-    float mraw = -INFINITY;   // max of the raw scores (scale > 0 commutes with max)
-    if (full) {
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) mraw = fmaxf(mraw, sacc[st][j]);
-      }
-    } else {
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-#pragma unroll
-        for (int jq = 0; jq < 4; ++jq) {
-          const int4 kp4 = *reinterpret_cast<const int4*>(skpos + 32 * st + 8 * jq + 4 * half);
-          const int kpv[4] = {kp4.x, kp4.y, kp4.z, kp4.w};
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            const int j = 4 * jq + jj;
-            const float v = kpv[jj] <= qpos ? sacc[st][j] : -INFINITY;
-            sacc[st][j] = v;
-            mraw = fmaxf(mraw, v);
-          }
-        }
-      }
-    }
-    mraw = fmaxf(mraw, __shfl_xor(mraw, 32));
-    const float mx = mraw * a.scale_log2;   // log2 units; -inf when nothing is visible
-    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleSlack) != 0) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = fast_exp2(m_run - m_new);
-      l_run *= alpha;
-      m_run = m_new;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) o[dt][j] *= alpha;
-      }
-    }
-    float psum = 0.0f;
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
+    if constexpr (decltype(maskc)::value) {
+      // visible: valid block, position < ctx and <= the row's position
+      const int lim = min(qpos, ctx - 1);
+      const bool ok0 = entry(2 * tile) >= 0, ok1 = entry(2 * tile + 1) >= 0;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const float p = fast_exp2(fmaf(sacc[st][j], a.scale_log2, -m_run));
-        sacc[st][j] = p;
-        psum += p;
+        const int k = 8 * (j >> 2) + 4 * half + (j & 3);   // j is a constant; half per lane
+        const int pos = 32 * tile + (k & 16) + slot_of_offset(k & 15, dirv);
+        const bool ok = (j >> 3) ? ok1 : ok0;   // k / 16 == j / 8
+        cur[j] = (ok && pos <= lim) ? cur[j] : -INFINITY;
       }
     }
-    l_run += psum;
-
-    // P^T operand for key step c2 (16 keys): accumulators 8*(c2%2) .. +8 of sub-tile c2/2.
-    bf16x8_t pf[4];
+    float mr = -INFINITY;   // max of the raw scores (the scale > 0 commutes with max)
 #pragma unroll
-    for (int c2 = 0; c2 < 4; ++c2) {
-      const floatx16& sv = sacc[c2 >> 1];
-      const int j0 = 8 * (c2 & 1);
-      uint4 pk;
-      pk.x = pack2_bf16(sv[j0 + 0], sv[j0 + 1]);
-      pk.y = pack2_bf16(sv[j0 + 2], sv[j0 + 3]);
-      pk.z = pack2_bf16(sv[j0 + 4], sv[j0 + 5]);
-      pk.w = pack2_bf16(sv[j0 + 6], sv[j0 + 7]);
+    for (int j = 0; j < 16; ++j) mr = fmaxf(mr, cur[j]);
+    const float mx = pair_max(mr) * sl2;   // log2 units; -inf when nothing is visible
+    const float m_new = mx > m_run + kRescaleSlack ? mx : m_run;
+    alpha = fast_exp2(m_run - m_new);
+    l_run *= alpha;
+    m_run = m_new;
+  };
+  // P = exp2(S * scale - m) rounded to bf16 (the P^T operands). l sums the
+  // rounded values (two per dot product with (1, 1)), i.e. exactly the
+  // weights the PV product applies. Operand c2 (16 keys) holds accumulators
+  // 8*c2 .. 8*c2 + 7.
+  const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
+  auto probs = [&](bf16x8_t (&pf)[2]) __attribute__((always_inline)) {
+    float psum = l_run;
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2) {
+      bf16x2_t pw[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float2_t pp = {fast_exp2(fmaf(cur[8 * c2 + 2 * w], sl2, -m_run)),
+                             fast_exp2(fmaf(cur[8 * c2 + 2 * w + 1], sl2, -m_run))};
+        pw[w] = __builtin_convertvector(pp, bf16x2_t);   // round to nearest even
+        // (the packed pair goes to the dot product as it is: taking it back
+        // out of a vector here has been miscompiled into the first pair)
+        psum = __builtin_amdgcn_fdot2_f32_bf16(pw[w], ones, psum, false);
+      }
+      const v4u_t pk = {__builtin_bit_cast(uint32_t, pw[0]), __builtin_bit_cast(uint32_t, pw[1]),
+                        __builtin_bit_cast(uint32_t, pw[2]), __builtin_bit_cast(uint32_t, pw[3])};
       pf[c2] = as_bf16x8(pk);
     }
-
-    // O^T += V^T P^T: V^T operand row d holds keys 16c2 + 4*half + {0..3} and
-    // 16c2 + 8 + 4*half + {0..3}, the same permutation the P operand carries.
+    l_run = psum;
+  };
+  // V^T operands of the tile in V ring `sv` for key step c2.
+  auto v_operands = [&](const uint8_t* sv, int c2, v4u_t (&vv)[4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
       // chunk 4dt + (2(j % 2) + q / 2) of the row: the dt bits XOR the swizzle's high bits
-      const int off0 = v_off[0] + (((4 * dt) ^ (v_sw[0] & 12)) << 4);
-      const int off1 = v_off[1] + (((4 * dt) ^ (v_sw[1] & 12)) << 4);
+      const uint2 lo = lds_read_tr(sv + 16 * c2 * kRowBytes + v_off[0] + (((4 * dt) ^ (v_sw[0] & 12)) << 4));
+      const uint2 hi = lds_read_tr(sv + 16 * c2 * kRowBytes + v_off[1] + (((4 * dt) ^ (v_sw[1] & 12)) << 4));
+      vv[dt] = v4u_t{lo.x, lo.y, hi.x, hi.y};
+    }
+  };
+  // O^T += V^T P^T for key step c2.
+  auto pv = [&](const v4u_t (&vv)[4], const bf16x8_t (&pf)[2], int c2) __attribute__((always_inline)) {
 #pragma unroll
-      for (int c2 = 0; c2 < 4; ++c2) {
-        const uint2 lo = lds_read_tr(sv + 16 * c2 * kRowBytes + off0);
-        const uint2 hi = lds_read_tr(sv + 16 * c2 * kRowBytes + off1);
-        const uint4 vv = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pf[c2], o[dt], 0, 0, 0);
-      }
+    for (int dt = 0; dt < 4; ++dt)
+      o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv[dt]), pf[c2], o[dt], 0, 0, 0);
+  };
+  // Rare (lazy max). Each accumulator is read, scaled and written back by one
+  // short sequence with its own temporary, so the rescale never stages all of
+  // O in vector registers. The compiler does not look inside these sequences
+  // for hazards, so the wait states a read of a matrix-core result needs (and
+  // a later matrix-core read of the rewritten values) are padded explicitly.
+  auto rescale_o = [&]() __attribute__((always_inline)) {
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          float tmp;
+          asm volatile("v_accvgpr_read_b32 %0, %1\n\tv_mul_f32 %0, %0, %2\n\tv_accvgpr_write_b32 %1, %0"
+                       : "=&v"(tmp), "+a"(o[dt][j])
+                       : "v"(alpha));
+        }
+      asm volatile("s_nop 7\n\ts_nop 7");
     }
   };
 
-  // Tile kt is computed from buffer kt % 2 while tile kt + 1 lands in the
-  // other; after the barrier that frees a buffer, the tile two ahead is
-  // requested into it, then this wave waits for its own loads of the next tile
-  // (every older load: eight per tile are younger), fixes it up, and a second
-  // barrier publishes it.
-  using Buf0 = std::integral_constant<int, 0>;
-  using Buf1 = std::integral_constant<int, 1>;
-  load_tile(0, Buf0{});
-  load_tile(1, Buf1{});
-  wait_vmem<8>();
-  fixup(0, Buf0{});
+  // One step of this wave: P and PV for its current tile (V in `sv`) and, when
+  // it has a next tile, that tile's scores (K in `sk`), mask (for tile
+  // `next_tile`) and max. Phases, kept apart by scheduling barriers: the LDS reads
+  // go first; then the next tile's score products run on the matrix cores
+  // while the vector ALU forms the current probabilities; then the PV
+  // products run while the new scores are moved, masked and maxed. The other
+  // wave on the SIMD fills the gaps.
+  auto step = [&](const uint8_t* sk, const uint8_t* sv, int next_tile, auto has_next, auto mask_next)
+                  __attribute__((always_inline)) {
+    constexpr bool NEXT = decltype(has_next)::value;
+    v4u_t kv[8];
+    v4u_t vv0[4], vv1[4];
+    if constexpr (NEXT) k_operands(sk, kv);
+    v_operands(sv, 0, vv0);
+    __builtin_amdgcn_sched_barrier(0);
+    bf16x8_t pf[2];
+    floatx16 acc;
+    if constexpr (NEXT) scores(kv, acc);
+    probs(pf);
+    v_operands(sv, 1, vv1);
+    __builtin_amdgcn_sched_barrier(0);
+    pv(vv0, pf, 0);
+    pv(vv1, pf, 1);
+    if constexpr (NEXT) mask_max(acc, mask_next, next_tile);
+  };
+  // After step ii: wait for batch ii + 1 (K of step ii + 2, V of step ii + 1),
+  // zero V's non-context rows (FIX; a tile below plain_tiles has none),
+  // publish, then issue batch ii + 4 into the slots step ii freed (K slot
+  // (ii + 1) % 4, V slot ii % 4). eF, eV, eK are this wave's table entries
+  // for steps ii + 1, ii + 4 and ii + 5.
+  auto advance = [&](int ii, int sl, int eF, int eV, int eK, auto fixc) __attribute__((always_inline)) {
+    const int sl1 = (sl + 1) & (kSlots - 1);
+    wait_vmem<2 * kLoadsPerStep>();
+    if constexpr (decltype(fixc)::value) fixup_v(ii + 1, eF, s_vring + sl1 * kSlotBytes);
+    lds_barrier();
+    issue(ii + 5, eK, kpool, s_kring + sl1 * kSlotBytes);
+    issue(ii + 4, eV, vpool, s_vring + sl * kSlotBytes);
+  };
+  const uint8_t* kr = s_kring + kh * kTileBytes;
+  const uint8_t* vr = s_vring + kh * kTileBytes;
+
+  // ---- Prologue. Step j's K tile lives in K slot j % 4, its V tile in V
+  // slot j % 4. Batch b = (K of step
+  // b + 1, V of step b) is issued after step b - 4 frees both slots. K of
+  // step 0 and batch 0 go first, together with Q; batches 1 .. 3 follow once
+  // the first scores are in. Table entries run ahead of their use in a
+  // window: w0 .. w4 hold this wave's entries for steps ii + 1 .. ii + 5.
+  const int e0 = own(0);
+  int w0 = own(1), w1 = own(2), w2 = own(3), w3 = own(4), w4 = own(5);
+  issue(0, e0, kpool, s_kring);
+  issue(1, w0, kpool, s_kring + 1 * kSlotBytes);
+  issue(0, e0, vpool, s_vring);
+  // Tiles below `plain_tiles` need no mask: every key is context, sits behind
+  // a valid table entry and is visible to every row of the unit. The first
+  // invalid entry comes from one pass over the sequence's table, while the
+  // first tiles are in flight.
+  if (tid == 0) s_first_bad = nblk;
+  __syncthreads();
+  for (int b = tid; b < nblk; b += kThreads) {
+    const int v = tbl[b];
+    if (v < 0 || v >= a.num_blocks) atomicMin(&s_first_bad, b);
+  }
+  __syncthreads();
+  const int first_bad = __builtin_amdgcn_readfirstlane(s_first_bad);
+  const int plain_tiles = min(full_below / kKeys, first_bad / 2);
+  // Everything so far, Q included: a wait the compiler sees, so it knows the
+  // Q registers are ready and adds no wait of its own later.
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+  fixup_v(0, e0, s_vring);
   lds_barrier();
-  for (int kt = 0; kt < n_tiles; kt += 2) {
-    compute(kt, Buf0{});
-    lds_barrier();
-    load_tile(kt + 2, Buf0{});
-    wait_vmem<8>();
-    fixup(kt + 1, Buf1{});
-    lds_barrier();
-    if (kt + 1 < n_tiles) compute(kt + 1, Buf1{});
-    lds_barrier();
-    load_tile(kt + 3, Buf1{});
-    wait_vmem<8>();
-    fixup(kt + 2, Buf0{});
-    lds_barrier();
+  if (n_mine > 0) {
+    v4u_t kv[8];
+    floatx16 acc;
+    k_operands(kr, kv);
+    scores(kv, acc);
+    if (kh >= plain_tiles) mask_max(acc, std::true_type{}, kh);
+    else mask_max(acc, std::false_type{}, kh);
+  }
+  lds_barrier();   // K slot 0 is free again
+  issue(2, w1, kpool, s_kring + 2 * kSlotBytes);
+  issue(1, w0, vpool, s_vring + 1 * kSlotBytes);
+  issue(3, w2, kpool, s_kring + 3 * kSlotBytes);
+  issue(2, w1, vpool, s_vring + 2 * kSlotBytes);
+  issue(4, w3, kpool, s_kring);
+  issue(3, w2, vpool, s_vring + 3 * kSlotBytes);
+
+  // ---- Steps. Before step i: batch i (K of step i + 1, V of step i) is in
+  // LDS, batches i + 1 .. i + 3 are in flight. The steady state (this wave has
+  // a next tile and it needs no mask) runs unrolled by the ring size, with
+  // the slots as constants; the rest (the tiles at the diagonal or the context
+  // end, a tile behind an invalid table entry, the last tile) runs in
+  // separate loops with the slot as a variable.
+  int ii = 0;
+  // The next entry of the window: requested at the start of a step, used
+  // from the next one on.
+  auto shift = [&](int nw) __attribute__((always_inline)) {
+    w0 = w1;
+    w1 = w2;
+    w2 = w3;
+    w3 = w4;
+    w4 = nw;
+  };
+  // this wave's tiles 2 j + kh below plain_tiles, as a step bound
+  const int n_plain = min(n_mine, (plain_tiles - kh + 1) / 2);
+  auto main_step = [&](auto uc) __attribute__((always_inline)) -> bool {
+    constexpr int u = decltype(uc)::value;
+    if (ii + 1 >= n_plain) return false;
+    const int nw = own(ii + 6);
+    step(kr + ((u + 1) % kSlots) * kSlotBytes, vr + u * kSlotBytes, 0, std::true_type{}, std::false_type{});
+    rescale_o();
+    advance(ii, u, w0, w3, w4, std::false_type{});
+    shift(nw);
+    ++ii;
+    return true;
+  };
+  while (main_step(Int<0>{}) && main_step(Int<1>{}) && main_step(Int<2>{}) && main_step(Int<3>{})) {
+  }
+  // Tiles with a next tile that needs (or may need) the mask.
+  for (; ii + 1 < n_mine; ++ii) {
+    const int sl = ii & (kSlots - 1);
+    const int sl1 = (sl + 1) & (kSlots - 1);
+    const int nw = own(ii + 6);
+    step(kr + sl1 * kSlotBytes, vr + sl * kSlotBytes, 2 * (ii + 1) + kh, std::true_type{}, std::true_type{});
+    rescale_o();
+    advance(ii, sl, w0, w3, w4, std::true_type{});
+    shift(nw);
+  }
+  // The last tile of this wave's half.
+  if (ii < n_mine) {
+    const int sl = ii & (kSlots - 1);
+    const int nw = own(ii + 6);
+    step(kr, vr + sl * kSlotBytes, 0, std::false_type{}, std::false_type{});
+    advance(ii, sl, w0, w3, w4, std::true_type{});
+    shift(nw);
+    ++ii;
+  }
+  // Steps where only the other half has a tile.
+  for (; ii < n_steps; ++ii) {
+    const int nw = own(ii + 6);
+    advance(ii, ii & (kSlots - 1), w0, w3, w4, std::true_type{});
+    shift(nw);
   }
 
-  // Each half-wave summed its own keys; the row total is their sum.
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (row_valid) {
-    const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
-    uint16_t* op = static_cast<uint16_t*>(a.out) + ((size_t)(q_begin + qrow) * Hq + head) * kHeadDim;
+  // ---- Merge the two key halves through LDS (K ring reused once every load
+  // has landed and every wave is past the last step) and write the rows.
+  wait_vmem<0>();
+  lds_barrier();
+  l_run = pair_sum(l_run);
+  float* xo = reinterpret_cast<float*>(s_kring + rg * kSlotBytes);   // per row group: [dt][jq][lane] float4 = 16 KB
+  float* xm = reinterpret_cast<float*>(s_vring);                     // [rg][m, l][lane]
+  if (kh == 1) {
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        const int d0 = 32 * dt + 8 * jq + 4 * half;   // accumulators 4jq..4jq+3 are dims d0..d0+3
-        uint2 w;
-        w.x = pack2_bf16(o[dt][4 * jq + 0] * inv, o[dt][4 * jq + 1] * inv);
-        w.y = pack2_bf16(o[dt][4 * jq + 2] * inv, o[dt][4 * jq + 3] * inv);
-        *reinterpret_cast<uint2*>(op + d0) = w;
+        const float4 v = make_float4(o[dt][4 * jq], o[dt][4 * jq + 1], o[dt][4 * jq + 2], o[dt][4 * jq + 3]);
+        *reinterpret_cast<float4*>(xo + ((dt * 4 + jq) * kWave + lane) * 4) = v;
+      }
+    xm[(rg * 2 + 0) * kWave + lane] = m_run;
+    xm[(rg * 2 + 1) * kWave + lane] = l_run;
+  }
+  lds_barrier();
+  if (kh == 0) {
+    const float m1x = xm[(rg * 2 + 0) * kWave + lane];
+    const float l1 = xm[(rg * 2 + 1) * kWave + lane];
+    const float m = fmaxf(m_run, m1x);
+    const float wt0 = fast_exp2(m_run - m), wt1 = fast_exp2(m1x - m);
+    const float l = l_run * wt0 + l1 * wt1;
+    const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+    const float f0 = wt0 * inv, f1 = wt1 * inv;
+    if (row_valid) {
+      uint16_t* op = static_cast<uint16_t*>(a.out) + row_off;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+        for (int jq = 0; jq < 4; ++jq) {
+          const float4 v1 = *reinterpret_cast<const float4*>(xo + ((dt * 4 + jq) * kWave + lane) * 4);
+          const int d0 = 32 * dt + 8 * jq + 4 * half;   // accumulators 4jq..4jq+3 are dims d0..d0+3
+          uint2 w;
+          w.x = pack2_bf16(o[dt][4 * jq + 0] * f0 + v1.x * f1, o[dt][4 * jq + 1] * f0 + v1.y * f1);
+          w.y = pack2_bf16(o[dt][4 * jq + 2] * f0 + v1.z * f1, o[dt][4 * jq + 3] * f0 + v1.w * f1);
+          *reinterpret_cast<uint2*>(op + d0) = w;
+        }
       }
     }
   }
@@ -394,7 +624,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a
 
 }  // namespace
 
-int prefill_positions_per_tile(int group) { return 128 / group; }
+int prefill_positions_per_tile(int group) { return kRows / group; }
 
 hipError_t launch_prefill_mfma(const PrefillArgs& a, int group, int num_tiles_total, hipStream_t stream) {
   if (num_tiles_total <= 0) return hipSuccess;
