@@ -66,6 +66,7 @@ constexpr int kRowBytes = kHeadDim * 2;            // bytes of one K or V row
 constexpr int kTileBytes = kKeys * kRowBytes;      // one K or V tile in LDS
 constexpr float kRescaleSlack = 8.0f;              // log2 units
 constexpr float kNoMax = -1.0e30f;
+constexpr int kMaxTableLds = kPrefillMaxCtxMfma / kBlockSize;   // table entries staged in LDS
 constexpr int kMaxRankItems = kThreads;            // units ranked by length on the device
 constexpr int kLoadsPerStep = 4;                   // two K and two V loads per wave per step
 
@@ -153,6 +154,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   __shared__ __attribute__((aligned(1024))) uint8_t s_kring[kSlots * kSlotBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t s_vring[kSlots * kSlotBytes];
   __shared__ int s_first_bad;
+  __shared__ int s_tbl[kMaxTableLds];   // the sequence's validated table entries (-1: invalid)
   __shared__ __attribute__((aligned(16))) int s_len[kMaxRankItems];
   __shared__ int s_item;
 
@@ -263,7 +265,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   };
   const int my_bt = rg >> 1;                // block of the tile holding this wave's rows
   const int my_slot0 = 8 * (rg & 1);        // first of its slots
-  auto own = [&](int j) -> int { return entry(2 * (2 * j + kh) + my_bt); };
+  // This wave's (validated) entry for step j, from the table staged in LDS.
+  // Read a step ahead of its use; the value comes back in a vector register
+  // and is made scalar where it is used.
+  auto own = [&](int j) -> int {
+    const int b = 2 * (2 * j + kh) + my_bt;
+    return b < nblk ? s_tbl[b] : -1;
+  };
+  auto valid = [&](int j, int v) -> int { return __builtin_amdgcn_readfirstlane(v); };
 
   // Loads: load i (0, 1) covers tile rows 8 rg + 4i + lane / 16, lane writing
   // physical chunk lane % 16, which holds logical chunk (lane % 16) ^ swz(row).
@@ -277,7 +286,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     const int row = 8 * rg + 4 * i + ld_slot;   // tile row
     ld_off[i] = (uint32_t)(((my_slot0 + 4 * i + ld_slot) * kHeadDim + (((lane & 15) ^ swz(row)) << 3)) * 2);
   }
-  auto issue = [&](int j, int blk, const uint16_t* pool, uint8_t* ring) __attribute__((always_inline)) {
+  auto issue = [&](int j, int raw, const uint16_t* pool, uint8_t* ring) __attribute__((always_inline)) {
+    const int blk = valid(j, raw);
     const int b = (2 * j + kh < n_kt && blk >= 0) ? blk : 0;
     const uint16_t* base = pool + ((size_t)b * Hkv + g) * kBlockSize * kHeadDim;
     uint8_t* dst = ring + kh * kTileBytes + 8 * rg * kRowBytes;
@@ -286,9 +296,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   };
   // Once this wave's V loads of step j have landed: zero its rows whose slot
   // is not context.
-  auto fixup_v = [&](int j, int blk, uint8_t* ring) __attribute__((always_inline)) {
+  auto fixup_v = [&](int j, int raw, uint8_t* ring) __attribute__((always_inline)) {
     const int tile = 2 * j + kh;
     if (tile >= n_kt) return;
+    const int blk = valid(j, raw);
     const int b = 2 * tile + my_bt;
     if (blk >= 0 && (b + 1) * kBlockSize <= ctx) return;
     uint8_t* dv = ring + kh * kTileBytes + 8 * rg * kRowBytes;
@@ -320,9 +331,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = floatx16{};
   float m_run = kNoMax, l_run = 0.0f, alpha = 1.0f;
-  // Raw scores of the wave's next tile in vector registers: read out of the
-  // accumulators once (by the max) and carried to the step that turns them
-  // into probabilities.
+  // Raw scores of the wave's next tile, carried from the step that computes
+  // them (and their max) to the step that turns them into probabilities.
+  // Every accumulator here lives in vector registers: with no accumulation
+  // register in use, the compiler gives the wave its whole register budget as
+  // vector registers and the matrix cores write their results there, so the
+  // vector ALU reads scores and rescales O directly.
   floatx16 cur;
   const float sl2 = a.scale_log2;
 
@@ -338,23 +352,19 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     for (int c = 0; c < 8; ++c)
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[c]), qf[c], c == 0 ? floatx16{} : acc, 0, 0, 0);
   };
-  // Move the accumulators to `cur`, mask them (when asked: `tile` is the
+  // Take the accumulators as `cur`, mask them (when asked: `tile` is the
   // tile they belong to) and fold the tile's max into the running max; sets
   // alpha, the factor O and l take for the new max. Accumulator j is key
   // k = 8*(j/4) + 4*half + j%4 of the tile: physical slot k % 16 of the
   // tile's block k / 16, which holds that block's position offset
   // slot_of_offset(k % 16, dir).
   auto mask_max = [&](floatx16& acc, auto maskc, int tile) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      float v = acc[j];
-      asm volatile("" : "+v"(v));
-      cur[j] = v;
-    }
+    cur = acc;
     if constexpr (decltype(maskc)::value) {
       // visible: valid block, position < ctx and <= the row's position
       const int lim = min(qpos, ctx - 1);
-      const bool ok0 = entry(2 * tile) >= 0, ok1 = entry(2 * tile + 1) >= 0;
+      const bool ok0 = (2 * tile < nblk ? s_tbl[2 * tile] : -1) >= 0;
+      const bool ok1 = (2 * tile + 1 < nblk ? s_tbl[2 * tile + 1] : -1) >= 0;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int k = 8 * (j >> 2) + 4 * half + (j & 3);   // j is a constant; half per lane
@@ -413,24 +423,11 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     for (int dt = 0; dt < 4; ++dt)
       o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv[dt]), pf[c2], o[dt], 0, 0, 0);
   };
-  // Rare (lazy max). Each accumulator is read, scaled and written back by one
-  // short sequence with its own temporary, so the rescale never stages all of
-  // O in vector registers. The compiler does not look inside these sequences
-  // for hazards, so the wait states a read of a matrix-core result needs (and
-  // a later matrix-core read of the rewritten values) are padded explicitly.
+  // Rare (lazy max).
   auto rescale_o = [&]() __attribute__((always_inline)) {
     if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
-      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          float tmp;
-          asm volatile("v_accvgpr_read_b32 %0, %1\n\tv_mul_f32 %0, %0, %2\n\tv_accvgpr_write_b32 %1, %0"
-                       : "=&v"(tmp), "+a"(o[dt][j])
-                       : "v"(alpha));
-        }
-      asm volatile("s_nop 7\n\ts_nop 7");
+      for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
     }
   };
 
@@ -481,8 +478,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   // step 0 and batch 0 go first, together with Q; batches 1 .. 3 follow once
   // the first scores are in. Table entries run ahead of their use in a
   // window: w0 .. w4 hold this wave's entries for steps ii + 1 .. ii + 5.
-  const int e0 = own(0);
-  int w0 = own(1), w1 = own(2), w2 = own(3), w3 = own(4), w4 = own(5);
+  // (the first entries as scalar loads: the LDS copy is made while they load)
+  auto own0 = [&](int j) -> int { return entry(2 * (2 * j + kh) + my_bt); };
+  const int e0 = own0(0);
+  int w0 = own0(1), w1 = own0(2), w2 = own0(3), w3 = own0(4), w4 = own0(5);
   issue(0, e0, kpool, s_kring);
   issue(1, w0, kpool, s_kring + 1 * kSlotBytes);
   issue(0, e0, vpool, s_vring);
@@ -494,7 +493,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   __syncthreads();
   for (int b = tid; b < nblk; b += kThreads) {
     const int v = tbl[b];
-    if (v < 0 || v >= a.num_blocks) atomicMin(&s_first_bad, b);
+    const bool ok = v >= 0 && v < a.num_blocks;
+    s_tbl[b] = ok ? v : -1;
+    if (!ok) atomicMin(&s_first_bad, b);
   }
   __syncthreads();
   const int first_bad = __builtin_amdgcn_readfirstlane(s_first_bad);
