@@ -141,6 +141,9 @@ def main():
     ap.add_argument("--workload", default="llama3-8b-mixed-step")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--overlap", action="store_true", help="run the prefill on a side stream beside the decode")
+    ap.add_argument("--prefill-cus", type=int, default=0,
+                    help="run the prefill on the first N compute units and the write and decode on the rest "
+                         "(N a multiple of 32; implies --overlap)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check", action="store_true", help="check the benchmarked step against the oracle first")
@@ -176,9 +179,9 @@ def main():
     batch = workload.generate(args.workload, seed=args.seed)
     bros.bros_check_batch(batch.block_tables, batch.dir, batch.cls, batch.ctx_lens, batch.num_blocks)
     dev = bros.to_device(batch)
-    step = MixedStep(batch, dev, overlap=args.overlap)
+    step = MixedStep(batch, dev, overlap=args.overlap, prefill_cus=args.prefill_cus)
     work = algorithmic_work(batch)
-    stream = torch.cuda.current_stream()
+    stream = step.main if step.main is not None else torch.cuda.current_stream()
 
     if args.check:
         sys.path.insert(0, os.path.join(ROOT, "tests"))
@@ -246,7 +249,7 @@ def main():
                    "prefill_chunks": batch.num_prefill, "decode_rows": batch.num_seqs - batch.num_prefill,
                    "q_heads": batch.num_q_heads, "kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim,
                    "block_size": 16, "pool_blocks": batch.num_blocks, "sum_ctx": int(batch.ctx_lens.sum()),
-                   "overlap": bool(step.overlap)},
+                   "overlap": bool(step.overlap), "prefill_cus": step.prefill_cus},
         "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
         "step_bytes": work["step_bytes"],
         "roofline": roof,
@@ -256,6 +259,7 @@ def main():
         tf = work["prefill"]["flops"] / (per_call["prefill"] * 1e-3) / 1e12
         line["prefill_mfma"] = {"achieved_tflops": round(tf, 1), "peak_tflops": BF16_MFMA_PEAK_TFLOPS,
                                 "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "flops": work["prefill"]["flops"]}
+    step.close()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget)
     print(json.dumps(line), flush=True)

@@ -197,6 +197,33 @@ size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
                                 int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);
 
 /*
+ * bros_stream_create_cu_share -- a stream whose kernels run on a fixed share
+ * of the current device's compute units.
+ *
+ * Defines: the executor of Sec. 6 hands the prefill rows and the decode rows
+ * of one batch to two different attention kernels. The first is bound by the
+ * matrix cores and the second by HBM bandwidth; two such streams let them run
+ * side by side on disjoint compute units (prefill on one share, decode on the
+ * rest). bros_attn_decode sizes its grid by the compute units of the stream it
+ * is given, so it fills a share exactly.
+ *
+ * The share is compute units [first_cu, first_cu + num_cus) in the order of a
+ * HIP CU mask. On MI355X the runtime deals that order to the 8 dies in turn
+ * and, within a die, to its 4 shader engines in turn, so a range whose start
+ * and length are multiples of 32 holds the same number of compute units on
+ * every die and engine. Other ranges are rejected (BROS_E_SHAPE): a grid
+ * dispatched evenly over engines with unequal shares leaves work queued
+ * behind the smaller ones. Also BROS_E_SHAPE: a range beyond the device's
+ * compute units; BROS_E_NULL: stream is NULL; BROS_E_HIP: the runtime refused
+ * the mask or applied a different one. On success *stream holds a new
+ * hipStream_t at the default priority, owned by the caller, who releases it
+ * with bros_stream_destroy; on failure *stream is NULL.
+ */
+int bros_stream_create_cu_share(int32_t first_cu, int32_t num_cus, void** stream);
+/* Destroys a stream made by bros_stream_create_cu_share (after its work ends). */
+int bros_stream_destroy(void* stream);
+
+/*
  * bros_check_batch -- full host-side consistency check of a batch's metadata.
  *
  * Defines: the invariant behind Sec. 5.2 (two requests sharing a block never

@@ -24,7 +24,7 @@ STATUS = {0: "BROS_OK", -1: "BROS_E_NULL", -2: "BROS_E_SHAPE", -3: "BROS_E_DTYPE
 
 EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_write",
             "bros_attn_decode", "bros_attn_prefill_chunk", "bros_attn_workspace_size",
-            "bros_check_batch"]
+            "bros_check_batch", "bros_stream_create_cu_share", "bros_stream_destroy"]
 
 
 class BrosError(RuntimeError):
@@ -58,6 +58,10 @@ def _load() -> ctypes.CDLL:
     lib.bros_attn_workspace_size.restype = Z
     lib.bros_check_batch.argtypes = [P, I, P, P, P, I, I, I, I]
     lib.bros_check_batch.restype = ctypes.c_int
+    lib.bros_stream_create_cu_share.argtypes = [I, I, ctypes.POINTER(ctypes.c_void_p)]
+    lib.bros_stream_create_cu_share.restype = ctypes.c_int
+    lib.bros_stream_destroy.argtypes = [P]
+    lib.bros_stream_destroy.restype = ctypes.c_int
     return lib
 
 
@@ -150,6 +154,19 @@ def bros_check_batch(block_tables: np.ndarray, dir, cls, ctx_lens: np.ndarray, n
     _check(LIB.bros_check_batch(_ptr(bt), int(bt.shape[1]) if bt.ndim == 2 else 0, _ptr(dr), _ptr(cs),
                                 _ptr(cl), int(cl.shape[0]), int(num_blocks), int(block_size),
                                 1 if check_slot_disjointness else 0))
+
+
+def bros_stream_create_cu_share(first_cu: int, num_cus: int):
+    """A torch stream wrapping a new hipStream_t limited to compute units
+    [first_cu, first_cu + num_cus); release it with bros_stream_destroy."""
+    import torch
+    handle = ctypes.c_void_p()
+    _check(LIB.bros_stream_create_cu_share(int(first_cu), int(num_cus), ctypes.byref(handle)))
+    return torch.cuda.ExternalStream(handle.value)
+
+
+def bros_stream_destroy(stream) -> None:
+    _check(LIB.bros_stream_destroy(ctypes.c_void_p(_stream(stream))))
 
 
 # ---------------------------------------------------------------------------

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <vector>
 
 namespace {
 
@@ -39,6 +40,9 @@ int check_meta(const char* fn, const void* block_tables, int32_t max_blocks_per_
   if (!aligned(block_tables, 4)) return fail(BROS_E_SHAPE, "%s: block_tables is not 4-byte aligned", fn);
   return BROS_OK;
 }
+
+// Compute units per step of a CU share: 8 dies x 4 shader engines.
+constexpr int kCuShareGranule = 32;
 
 int launch_status(const char* fn, hipError_t e) {
   if (e != hipSuccess) return fail(BROS_E_HIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
@@ -221,6 +225,44 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   a.scale_log2 = scale_log2;
   bros::set_decode_workspace(a, need > 0 ? workspace : nullptr, bf16);
   return launch_status(fn, bros::launch_decode(a, group, bf16, s));
+}
+
+int bros_stream_create_cu_share(int32_t first_cu, int32_t num_cus, void** stream) {
+  const char* fn = "bros_stream_create_cu_share";
+  if (stream == nullptr) return fail(BROS_E_NULL, "%s: stream is NULL", fn);
+  *stream = nullptr;
+  if (first_cu < 0 || num_cus <= 0 || first_cu % kCuShareGranule != 0 || num_cus % kCuShareGranule != 0)
+    return fail(BROS_E_SHAPE, "%s: share [%d, %d + %d) must start and span multiples of %d compute units", fn,
+                first_cu, first_cu, num_cus, kCuShareGranule);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return fail(BROS_E_HIP, "%s: %s", fn, hipGetErrorString(e));
+  if ((int64_t)first_cu + num_cus > cus)
+    return fail(BROS_E_SHAPE, "%s: share [%d, %d) exceeds the device's %d compute units", fn, first_cu,
+                first_cu + num_cus, cus);
+  const size_t words = ((size_t)cus + 31) / 32;
+  std::vector<uint32_t> want(words, 0u), got(words, 0u);
+  for (int i = first_cu; i < first_cu + num_cus; ++i) want[i / 32] |= 1u << (i % 32);
+  hipStream_t s = nullptr;
+  e = hipExtStreamCreateWithCUMask(&s, (uint32_t)words, want.data());
+  if (e != hipSuccess) return fail(BROS_E_HIP, "%s: hipExtStreamCreateWithCUMask: %s", fn, hipGetErrorString(e));
+  e = hipExtStreamGetCUMask(s, (uint32_t)words, got.data());
+  if (e != hipSuccess || got != want) {
+    (void)hipStreamDestroy(s);
+    return fail(BROS_E_HIP, "%s: the runtime applied a different CU mask (%s)", fn,
+                e != hipSuccess ? hipGetErrorString(e) : "mask differs");
+  }
+  *stream = s;
+  return ok();
+}
+
+int bros_stream_destroy(void* stream) {
+  const char* fn = "bros_stream_destroy";
+  if (stream == nullptr) return fail(BROS_E_NULL, "%s: stream is NULL", fn);
+  const hipError_t e = hipStreamDestroy(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(BROS_E_HIP, "%s: %s", fn, hipGetErrorString(e));
+  return ok();
 }
 
 }  // extern "C"

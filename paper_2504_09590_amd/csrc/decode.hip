@@ -421,21 +421,49 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void decode_mfma_merge_kernel(
 
 }  // namespace
 
-int resident_workgroups(const void* kernel, int threads, int slot) {
+namespace {
+
+// Compute units enabled for `stream`: the population count of its CU mask, or
+// `fallback` when the mask cannot be read.
+int stream_cus(hipStream_t stream, int fallback) {
+  constexpr int kMaskWords = 32;   // up to 1024 CUs
+  uint32_t mask[kMaskWords] = {};
+  if (hipExtStreamGetCUMask(stream, kMaskWords, mask) != hipSuccess) {
+    (void)hipGetLastError();
+    return fallback;
+  }
+  int n = 0;
+  for (int i = 0; i < kMaskWords; ++i) n += __builtin_popcount(mask[i]);
+  return (n > 0 && n < fallback) ? n : fallback;
+}
+
+}  // namespace
+
+int resident_workgroups(const void* kernel, int threads, int slot, hipStream_t stream) {
   constexpr int kMaxDevices = 64;
   constexpr int kSlots = 8;
-  static int cache[kMaxDevices][kSlots];
+  static int per_cu_cache[kMaxDevices][kSlots];
+  static int cus_cache[kMaxDevices];
   static std::mutex mu;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 1024;
-  std::lock_guard<std::mutex> lock(mu);
-  if (cache[dev][slot] == 0) {
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess || per_cu <= 0) per_cu = 4;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
-    cache[dev][slot] = per_cu * cus;
+  int per_cu = 0, cus = 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (per_cu_cache[dev][slot] == 0) {
+      int n = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n <= 0) n = 4;
+      per_cu_cache[dev][slot] = n;
+    }
+    if (cus_cache[dev] == 0) {
+      int n = 0;
+      if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+      cus_cache[dev] = n;
+    }
+    per_cu = per_cu_cache[dev][slot];
+    cus = cus_cache[dev];
   }
-  return cache[dev][slot];
+  return per_cu * stream_cus(stream, cus);
 }
 
 namespace {
@@ -446,7 +474,7 @@ constexpr int kMaxDecodeGrid = 1024;
 
 template <int G>
 hipError_t launch_group(DecodeArgs a, hipStream_t stream, int slot) {
-  int grid = resident_workgroups(reinterpret_cast<const void*>(&decode_mfma_kernel<G>), kThreads, slot);
+  int grid = resident_workgroups(reinterpret_cast<const void*>(&decode_mfma_kernel<G>), kThreads, slot, stream);
   grid = grid < kMaxDecodeGrid ? grid : kMaxDecodeGrid;
   a.num_workers = grid * kWaves;
   hipLaunchKernelGGL((decode_mfma_kernel<G>), dim3(grid), dim3(kThreads), 0, stream, a);

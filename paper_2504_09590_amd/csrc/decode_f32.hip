@@ -520,7 +520,7 @@ __global__ __launch_bounds__(kHeadDim) void decode_f32_merge_kernel(DecodeArgs a
 template <int G>
 hipError_t launch_group_f32(const DecodeArgs& a, hipStream_t stream, int slot) {
   const long long padded = (long long)a.num_rows * a.num_kv_heads * a.n_split_max;
-  const int resident = resident_workgroups(reinterpret_cast<const void*>(&decode_f32_kernel<G>), kThreads, slot);
+  const int resident = resident_workgroups(reinterpret_cast<const void*>(&decode_f32_kernel<G>), kThreads, slot, stream);
   const int grid = (int)(padded < resident ? padded : resident);
   if (grid <= 0) return hipSuccess;
   hipLaunchKernelGGL((decode_f32_kernel<G>), dim3(grid), dim3(kThreads), 0, stream, a);

@@ -12,6 +12,9 @@ Order of one step:  bros_kv_write (all S sequences' new tokens)
                     -> bros_attn_decode (sequences [P, S)).
 With overlap=True the prefill runs on a second stream after the write, beside
 the decode, so the matrix-core bound and the HBM bound halves share the chip.
+With prefill_cus=N the two halves also get disjoint compute units: the
+prefill runs on a stream limited to the first N compute units, the write and
+the decode on a stream limited to the rest (N a multiple of 32).
 """
 
 from __future__ import annotations
@@ -23,7 +26,7 @@ from . import bros
 
 
 class MixedStep:
-    def __init__(self, batch, dev: bros.DeviceBatch, overlap: bool = False):
+    def __init__(self, batch, dev: bros.DeviceBatch, overlap: bool = False, prefill_cus: int = 0):
         self.batch = batch
         self.dev = dev
         P, S = batch.num_prefill, batch.num_seqs
@@ -41,10 +44,27 @@ class MixedStep:
         device = dev.k_pool.device
         self.ws_decode = torch.empty(max(ws_dec, 16), dtype=torch.uint8, device=device) if ws_dec else None
         self.ws_prefill = torch.empty(max(ws_pre, 16), dtype=torch.uint8, device=device) if ws_pre else None
-        self.overlap = overlap and P > 0 and S > P
-        self.side = torch.cuda.Stream(device=device) if self.overlap else None
+        self.prefill_cus = int(prefill_cus) if P > 0 and S > P else 0
+        self.overlap = (overlap or self.prefill_cus > 0) and P > 0 and S > P
+        self.main = None   # None: the caller's current stream
+        if self.prefill_cus:
+            total = torch.cuda.get_device_properties(device).multi_processor_count
+            self.side = bros.bros_stream_create_cu_share(0, self.prefill_cus)
+            self.main = bros.bros_stream_create_cu_share(self.prefill_cus, total - self.prefill_cus)
+        else:
+            self.side = torch.cuda.Stream(device=device) if self.overlap else None
         self._ev_written = torch.cuda.Event() if self.overlap else None
         self._ev_prefilled = torch.cuda.Event() if self.overlap else None
+        self._ev_enter = torch.cuda.Event()
+        self._ev_leave = torch.cuda.Event()
+
+    def close(self):
+        """Releases the compute-unit share streams (after their work is done)."""
+        if self.prefill_cus and self.main is not None:
+            torch.cuda.synchronize()
+            bros.bros_stream_destroy(self.side)
+            bros.bros_stream_destroy(self.main)
+            self.main = self.side = None
 
     # the three calls --------------------------------------------------------
     def kv_write(self, stream=None):
@@ -71,7 +91,11 @@ class MixedStep:
     def run(self, write: bool = True):
         """Enqueue one whole step on the current stream (plus the side stream
         when overlapping); returns (prefill output, decode output)."""
-        main = torch.cuda.current_stream()
+        cur = torch.cuda.current_stream()
+        main = self.main if self.main is not None else cur
+        if main is not cur:
+            self._ev_enter.record(cur)
+            main.wait_event(self._ev_enter)
         if write:
             self.kv_write(main)
         if self.overlap:
@@ -84,4 +108,7 @@ class MixedStep:
         else:
             self.prefill(main)
             self.decode(main)
+        if main is not cur:
+            self._ev_leave.record(main)
+            cur.wait_event(self._ev_leave)
         return self.out_prefill, self.out_decode

@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings_and_version():
     for code, name in bros.STATUS.items():
         assert bros.LIB.bros_status_str(code).decode() == name
-    assert bros.LIB.bros_abi_version() == 1
+    assert bros.LIB.bros_abi_version() == 2
 
 
 # --- argument validation (returns before any HIP call) -----------------------
@@ -108,6 +108,19 @@ def test_prefill_rejects():
     assert L.bros_attn_prefill_chunk(*a) == -5
     a = list(base); a[3] = 0
     assert L.bros_attn_prefill_chunk(*a) == 0
+
+
+@pytest.mark.parametrize("first,num", [(0, 0), (0, 48), (16, 32), (-32, 64), (0, -32)])
+def test_cu_share_rejects_uneven_ranges(first, num):
+    out = ctypes.c_void_p(123)
+    assert bros.LIB.bros_stream_create_cu_share(first, num, ctypes.byref(out)) == -2
+    assert out.value is None
+    assert "multiples of 32" in bros.LIB.bros_last_error().decode()
+
+
+def test_cu_share_rejects_null_outputs():
+    assert bros.LIB.bros_stream_create_cu_share(0, 32, None) == -1
+    assert bros.LIB.bros_stream_destroy(None) == -1
 
 
 def test_workspace_query():

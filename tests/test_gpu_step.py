@@ -1,6 +1,8 @@
 """One whole mixed step (kv_write -> prefill -> decode) through MixedStep, the
 dispatch the benchmark times, on the full mixed-step workload, against the
-oracle's step; with and without the prefill on a side stream."""
+oracle's step; with and without the prefill on a side stream, and with the
+two halves on disjoint compute-unit shares (which also checks that the decode
+grid fits a share)."""
 
 import numpy as np
 import pytest
@@ -17,17 +19,18 @@ def mixed():
     return b, oracle_step(b)
 
 
-@pytest.mark.parametrize("overlap", [False, True])
-def test_mixed_step_full(mixed, overlap):
+@pytest.mark.parametrize("overlap,prefill_cus", [(False, 0), (True, 0), (True, 64), (True, 224)])
+def test_mixed_step_full(mixed, overlap, prefill_cus):
     torch = require_gpu()
     from paper_2504_09590_amd import bros
     from paper_2504_09590_amd.step import MixedStep
     b, (k1, v1, pre_ref, dec_ref) = mixed
     dev = bros.to_device(b)
-    step = MixedStep(b, dev, overlap=overlap)
-    announce(f"mixed step {b.name} overlap={overlap}")
+    announce(f"mixed step {b.name} overlap={overlap} prefill_cus={prefill_cus}")
+    step = MixedStep(b, dev, overlap=overlap, prefill_cus=prefill_cus)
     pre, dec = step.run()
     torch.cuda.synchronize()
+    step.close()
     for name, ref, got in (("k", k1, dev.k_pool), ("v", v1, dev.v_pool)):
         assert np.array_equal(bros.to_host_bits(got), ref), f"{name} pool after the step"
     mx_p, mean_p = compare(bros.to_host_bits(pre), pre_ref, "bf16", "step prefill")
