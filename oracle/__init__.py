@@ -8,3 +8,6 @@ from .paged_attention import (  # noqa: F401
     softmax_attention, default_scale, kv_write, decode, prefill_chunk, owned_slots,
     slot_owner_counts,
 )
+from .checkpoint import (  # noqa: F401
+    slot_ids, kv_gather, kv_scatter, overwritten_peer_tokens,
+)
