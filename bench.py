@@ -133,6 +133,42 @@ def cpu_baseline(batch, budget_s: float):
             "sample": "; ".join(desc) + f"; {dt:.1f} s fp64 NumPy", "seconds": round(dt, 2)}
 
 
+def swap_figures(step, per_call, K):
+    """Lazy-checkpoint figures: the gather/scatter kernels inside the step, and
+    the host copies of the same rows (copy engine) timed alone, K of each."""
+    import torch
+    lane, n = step.swap, int(step.swap_ids.numel())
+    row = lane.out_k[0].numel() * lane.out_k.element_size()          # one slot, one tensor, all heads
+    moved = 2 * n * row                                              # K and V, each way
+    rates = {}
+    from paper_2504_09590_amd import bros
+    cs = lane.copy if lane.copy is not None else torch.cuda.current_stream()
+    for name, pairs in (("d2h", ((step.host_out_k, lane.out_k), (step.host_out_v, lane.out_v))),
+                        ("h2d", ((lane.in_k, step.host_in_k), (lane.in_v, step.host_in_v)))):
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(cs)
+        for _ in range(K):
+            for dst, src in pairs:
+                bros.bros_copy_dma(dst, src, moved // 2, stream=cs)
+        b.record(cs)
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) / K * 1e3
+        rates[name] = {"us": round(us, 2), "GB/s": round(moved / (us * 1e-6) / 1e9, 1)}
+    in_step = {}
+    for kind in ("d2h", "h2d"):
+        us = [a.elapsed_time(b) * 1e3 for k, a, b in lane.timing if k == kind]
+        if us:
+            in_step[kind] = {"us": round(float(np.mean(us)), 2), "GB/s": round(moved / (np.mean(us) * 1e-6) / 1e9, 1)}
+    lane.timing = None
+    g, sc = per_call["swap_gather"] * 1e3, per_call["swap_scatter"] * 1e3
+    return {"slots": n, "bytes_each_way": moved,
+            "gather_us": round(g, 2), "scatter_us": round(sc, 2),
+            "gather_hbm_GBps": round(2 * moved / (g * 1e-6) / 1e9, 1),
+            "scatter_hbm_GBps": round(2 * moved / (sc * 1e-6) / 1e9, 1),
+            "copies_in_step": in_step, "copies_alone": rates}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -144,6 +180,14 @@ def main():
     ap.add_argument("--prefill-cus", type=int, default=0,
                     help="run the prefill on the first N compute units and the write and decode on the rest "
                          "(N a multiple of 32; implies --overlap)")
+    ap.add_argument("--copy-cus", type=int, default=0,
+                    help="with --swap-slots: run the host copies on the first N compute units and the step on the "
+                         "rest (N a multiple of 32)")
+    ap.add_argument("--swap-serial", action="store_true",
+                    help="with --swap-slots: enqueue the host copies on the step's stream between its kernels")
+    ap.add_argument("--swap-slots", type=int, default=0,
+                    help="also checkpoint and restore N slots per step (lazy checkpointing), the host copies "
+                         "overlapping the attention")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check", action="store_true", help="check the benchmarked step against the oracle first")
@@ -179,7 +223,8 @@ def main():
     batch = workload.generate(args.workload, seed=args.seed)
     bros.bros_check_batch(batch.block_tables, batch.dir, batch.cls, batch.ctx_lens, batch.num_blocks)
     dev = bros.to_device(batch)
-    step = MixedStep(batch, dev, overlap=args.overlap, prefill_cus=args.prefill_cus)
+    step = MixedStep(batch, dev, overlap=args.overlap, prefill_cus=args.prefill_cus, swap_slots=args.swap_slots,
+                     copy_cus=args.copy_cus, swap_serial=args.swap_serial)
     work = algorithmic_work(batch)
     stream = step.main if step.main is not None else torch.cuda.current_stream()
 
@@ -200,19 +245,27 @@ def main():
 
     K = args.steps
     ev = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
-          for k in ("kv_write", "prefill", "decode")}
+          for k in ("kv_write", "prefill", "decode") + (("swap_gather", "swap_scatter") if step.swap else ())}
     written = [torch.cuda.Event() for _ in range(K)]
     prefilled = [torch.cuda.Event() for _ in range(K)]
     side = step.side if step.overlap else stream
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if step.swap:
+        step.swap.timing = []
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
     for i in range(K):
         # one step: kv_write, then prefill (on the side stream when overlapping) and decode;
         # every call is bracketed by events on the stream it runs on
+        if step.swap:
+            a, b = ev["swap_gather"][i]
+            a.record(stream); step.swap_out(stream); b.record(stream)
         a, b = ev["kv_write"][i]
         a.record(stream); step.kv_write(stream); b.record(stream)
+        if step.swap:
+            a, b = ev["swap_scatter"][i]
+            a.record(stream); step.swap_in(stream); b.record(stream)
         if step.overlap:
             written[i].record(stream)
             side.wait_event(written[i])
@@ -223,6 +276,8 @@ def main():
         if step.overlap:
             prefilled[i].record(side)
             stream.wait_event(prefilled[i])
+        if step.swap:
+            step.swap_next(stream)
     end.record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall) * 1e3
@@ -249,7 +304,9 @@ def main():
                    "prefill_chunks": batch.num_prefill, "decode_rows": batch.num_seqs - batch.num_prefill,
                    "q_heads": batch.num_q_heads, "kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim,
                    "block_size": 16, "pool_blocks": batch.num_blocks, "sum_ctx": int(batch.ctx_lens.sum()),
-                   "overlap": bool(step.overlap), "prefill_cus": step.prefill_cus},
+                   "overlap": bool(step.overlap), "prefill_cus": step.prefill_cus,
+                   "swap_slots": args.swap_slots, "copy_cus": step.copy_cus,
+                   "swap_serial": bool(args.swap_serial)},
         "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
         "step_bytes": work["step_bytes"],
         "roofline": roof,
@@ -259,6 +316,8 @@ def main():
         tf = work["prefill"]["flops"] / (per_call["prefill"] * 1e-3) / 1e12
         line["prefill_mfma"] = {"achieved_tflops": round(tf, 1), "peak_tflops": BF16_MFMA_PEAK_TFLOPS,
                                 "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "flops": work["prefill"]["flops"]}
+    if step.swap:
+        line["swap"] = swap_figures(step, per_call, K)
     step.close()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget)

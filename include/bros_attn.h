@@ -197,6 +197,74 @@ size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
                                 int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);
 
 /*
+ * bros_kv_gather / bros_kv_scatter -- lazy checkpointing of shared blocks.
+ *
+ * Defines: Sec. 5.2 (lazy checkpointing): once a shared block has no empty
+ * slot left, only the tokens of the peer request that a write is about to
+ * overwrite are copied to CPU memory, and they are copied back when that
+ * request is scheduled again; Sec. 6: dedicated kernels fetch and store KV
+ * in non-contiguous GPU memory and separate streams carry the host copies.
+ *
+ * A slot is named by its id, block * 16 + slot. For i in [0, num_slots) and
+ * every KV head h:
+ *   gather:   k_out[i][h][:] = k_pool[id_i / 16][h][id_i % 16][:]  (v likewise);
+ *             a row whose id lies outside [0, num_blocks * 16) is written as zeros.
+ *   scatter:  k_pool[id_i / 16][h][id_i % 16][:] = k_in[i][h][:]    (v likewise);
+ *             an id outside the pool is skipped. Ids inside the pool must be
+ *             distinct (repeated ids race; bros_check_slot_ids finds them).
+ * Dense buffers k_out/v_out/k_in/v_in: [num_slots][num_kv_heads][head_dim] in
+ * the pools' dtype, the layout of kv_write's new tokens. slot_ids: int32
+ * [num_slots] device array. Bytes move unchanged (bit-exact).
+ *
+ * The dense buffers are device memory, or pinned host memory the device can
+ * address (the kernel then runs at host-link speed and holds compute units
+ * meanwhile). The intended use is a device staging buffer plus an
+ * asynchronous copy on another stream: gather before the write that
+ * overwrites the slots, then copy device-to-host while attention runs; copy
+ * host-to-device ahead of time, then scatter before the attention that reads
+ * the restored slots.
+ *
+ * Errors: BROS_E_NULL (a pointer NULL with num_slots > 0), BROS_E_SHAPE
+ * (negative counts, num_blocks <= 0, num_kv_heads <= 0, misaligned tensors),
+ * BROS_E_DTYPE, BROS_E_UNSUPPORTED (block_size != 16, head_dim != 128).
+ * num_slots == 0 launches nothing.
+ */
+int bros_kv_gather(const void* k_pool, const void* v_pool, int32_t num_blocks,
+                   const int32_t* slot_ids, int32_t num_slots,
+                   void* k_out, void* v_out,
+                   int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                   int32_t dtype, void* stream);
+int bros_kv_scatter(const void* k_in, const void* v_in,
+                    const int32_t* slot_ids, int32_t num_slots,
+                    void* k_pool, void* v_pool, int32_t num_blocks,
+                    int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                    int32_t dtype, void* stream);
+
+/*
+ * bros_copy_dma -- an asynchronous copy of `bytes` bytes on a DMA engine.
+ *
+ * Defines: the host copies of Sec. 5.2's lazy checkpointing, carried on their
+ * own streams (Sec. 6). The copy runs on a copy engine, not on compute units,
+ * so it proceeds beside kernels that occupy every compute unit (a copy made
+ * as a kernel would queue behind them or take units from them). dst and src
+ * are device memory or pinned host memory (hipHostMalloc, or torch's
+ * pin_memory); the ranges must not overlap. Enqueued on `stream`; returns
+ * BROS_OK, BROS_E_NULL (a NULL pointer with bytes > 0) or BROS_E_HIP.
+ * Copies in both directions at once share the host link badly on MI355X
+ * (each falls to about a third of its rate alone), so one stream carrying
+ * both directions in turn is the faster arrangement.
+ */
+int bros_copy_dma(void* dst, const void* src, size_t bytes, void* stream);
+
+/*
+ * bros_check_slot_ids -- host-side check of a scatter's slot list: every id
+ * inside [0, num_blocks * 16) appears once. slot_ids is a HOST pointer.
+ * Returns BROS_OK or BROS_E_TABLE naming the first repeated id (BROS_E_NULL /
+ * BROS_E_SHAPE for bad arguments).
+ */
+int bros_check_slot_ids(const int32_t* slot_ids, int32_t num_slots, int32_t num_blocks);
+
+/*
  * bros_stream_create_cu_share -- a stream whose kernels run on a fixed share
  * of the current device's compute units.
  *

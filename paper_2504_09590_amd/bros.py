@@ -24,7 +24,8 @@ STATUS = {0: "BROS_OK", -1: "BROS_E_NULL", -2: "BROS_E_SHAPE", -3: "BROS_E_DTYPE
 
 EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_write",
             "bros_attn_decode", "bros_attn_prefill_chunk", "bros_attn_workspace_size",
-            "bros_check_batch", "bros_stream_create_cu_share", "bros_stream_destroy"]
+            "bros_check_batch", "bros_stream_create_cu_share", "bros_stream_destroy",
+            "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma"]
 
 
 class BrosError(RuntimeError):
@@ -62,6 +63,14 @@ def _load() -> ctypes.CDLL:
     lib.bros_stream_create_cu_share.restype = ctypes.c_int
     lib.bros_stream_destroy.argtypes = [P]
     lib.bros_stream_destroy.restype = ctypes.c_int
+    lib.bros_kv_gather.argtypes = [P, P, I, P, I, P, P, I, I, I, I, P]
+    lib.bros_kv_gather.restype = ctypes.c_int
+    lib.bros_kv_scatter.argtypes = [P, P, P, I, P, P, I, I, I, I, I, P]
+    lib.bros_kv_scatter.restype = ctypes.c_int
+    lib.bros_check_slot_ids.argtypes = [P, I, I]
+    lib.bros_check_slot_ids.restype = ctypes.c_int
+    lib.bros_copy_dma.argtypes = [P, P, Z, P]
+    lib.bros_copy_dma.restype = ctypes.c_int
     return lib
 
 
@@ -154,6 +163,39 @@ def bros_check_batch(block_tables: np.ndarray, dir, cls, ctx_lens: np.ndarray, n
     _check(LIB.bros_check_batch(_ptr(bt), int(bt.shape[1]) if bt.ndim == 2 else 0, _ptr(dr), _ptr(cs),
                                 _ptr(cl), int(cl.shape[0]), int(num_blocks), int(block_size),
                                 1 if check_slot_disjointness else 0))
+
+
+def bros_kv_gather(k_pool, v_pool, slot_ids, k_out, v_out, num_slots: int | None = None, stream=None):
+    """Rows of the pools at slot ids (block * 16 + slot) into dense [n][Hkv][D]
+    buffers (device memory, or pinned host memory). n defaults to len(slot_ids)."""
+    n = _numel0(slot_ids) if num_slots is None else int(num_slots)
+    nb, hkv, _, d = k_pool.shape
+    _check(LIB.bros_kv_gather(_ptr(k_pool), _ptr(v_pool), int(nb), _ptr(slot_ids), n, _ptr(k_out), _ptr(v_out),
+                              int(hkv), int(d), 16, _dtype_code(k_pool), _stream(stream)))
+
+
+def bros_kv_scatter(k_in, v_in, slot_ids, k_pool, v_pool, num_slots: int | None = None, stream=None):
+    """Dense [n][Hkv][D] rows back into the pools at slot ids; ids outside the
+    pool are skipped."""
+    n = _numel0(slot_ids) if num_slots is None else int(num_slots)
+    nb, hkv, _, d = k_pool.shape
+    _check(LIB.bros_kv_scatter(_ptr(k_in), _ptr(v_in), _ptr(slot_ids), n, _ptr(k_pool), _ptr(v_pool), int(nb),
+                               int(hkv), int(d), 16, _dtype_code(k_pool), _stream(stream)))
+
+
+def bros_copy_dma(dst, src, nbytes: int | None = None, stream=None) -> None:
+    """Asynchronous copy on a DMA engine between device and/or pinned host
+    tensors (contiguous); nbytes defaults to the size of src."""
+    n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
+    if n > dst.numel() * dst.element_size() or n > src.numel() * src.element_size():
+        raise ValueError("copy larger than a buffer")
+    _check(LIB.bros_copy_dma(_ptr(dst), _ptr(src), n, _stream(stream)))
+
+
+def bros_check_slot_ids(slot_ids: np.ndarray, num_blocks: int) -> None:
+    """Host check that the ids inside the pool are distinct; raises BrosError."""
+    ids = np.ascontiguousarray(slot_ids, dtype=np.int32)
+    _check(LIB.bros_check_slot_ids(_ptr(ids), int(ids.shape[0]), int(num_blocks)))
 
 
 def bros_stream_create_cu_share(first_cu: int, num_cus: int):

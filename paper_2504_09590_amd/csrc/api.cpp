@@ -227,6 +227,56 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   return launch_status(fn, bros::launch_decode(a, group, bf16, s));
 }
 
+static int kv_move(const char* fn, bool gather, void* k_pool, void* v_pool, int32_t num_blocks,
+                   const int32_t* slot_ids, int32_t num_slots, void* k_dense, void* v_dense,
+                   int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t dtype, void* stream) {
+  int group = 0;
+  int st = check_shapes(fn, num_kv_heads, num_kv_heads, head_dim, block_size, dtype, &group);
+  if (st) return st;
+  if (num_slots < 0) return fail(BROS_E_SHAPE, "%s: negative num_slots %d", fn, num_slots);
+  if (num_slots == 0) return ok();
+  if (num_blocks <= 0) return fail(BROS_E_SHAPE, "%s: num_blocks %d must be positive", fn, num_blocks);
+  if (!k_pool || !v_pool || !k_dense || !v_dense || !slot_ids)
+    return fail(BROS_E_NULL, "%s: a pool, dense buffer or slot_ids pointer is NULL", fn);
+  if (!aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(k_dense, 16) || !aligned(v_dense, 16) ||
+      !aligned(slot_ids, 4))
+    return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
+  bros::KvMoveArgs a{k_pool, v_pool, k_dense, v_dense, slot_ids, num_slots, num_blocks, num_kv_heads,
+                     head_dim * (dtype == BROS_BF16 ? 2 : 4)};
+  const hipError_t e = bros::launch_kv_move(a, gather, static_cast<hipStream_t>(stream));
+  if (e == hipErrorInvalidValue) return fail(BROS_E_SHAPE, "%s: %d slots make a grid too large", fn, num_slots);
+  return launch_status(fn, e);
+}
+
+int bros_kv_gather(const void* k_pool, const void* v_pool, int32_t num_blocks,
+                   const int32_t* slot_ids, int32_t num_slots,
+                   void* k_out, void* v_out,
+                   int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                   int32_t dtype, void* stream) {
+  return kv_move("bros_kv_gather", true, const_cast<void*>(k_pool), const_cast<void*>(v_pool), num_blocks,
+                 slot_ids, num_slots, k_out, v_out, num_kv_heads, head_dim, block_size, dtype, stream);
+}
+
+int bros_kv_scatter(const void* k_in, const void* v_in,
+                    const int32_t* slot_ids, int32_t num_slots,
+                    void* k_pool, void* v_pool, int32_t num_blocks,
+                    int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                    int32_t dtype, void* stream) {
+  return kv_move("bros_kv_scatter", false, k_pool, v_pool, num_blocks, slot_ids, num_slots,
+                 const_cast<void*>(k_in), const_cast<void*>(v_in), num_kv_heads, head_dim, block_size, dtype, stream);
+}
+
+int bros_copy_dma(void* dst, const void* src, size_t bytes, void* stream) {
+  const char* fn = "bros_copy_dma";
+  if (bytes == 0) return ok();
+  if (dst == nullptr || src == nullptr) return fail(BROS_E_NULL, "%s: dst or src is NULL", fn);
+  // The no-compute-unit kind makes the runtime use a copy engine for any pair
+  // of device-addressable ranges, pinned host memory included.
+  const hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDeviceNoCU, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(BROS_E_HIP, "%s: hipMemcpyAsync of %zu bytes: %s", fn, bytes, hipGetErrorString(e));
+  return ok();
+}
+
 int bros_stream_create_cu_share(int32_t first_cu, int32_t num_cus, void** stream) {
   const char* fn = "bros_stream_create_cu_share";
   if (stream == nullptr) return fail(BROS_E_NULL, "%s: stream is NULL", fn);

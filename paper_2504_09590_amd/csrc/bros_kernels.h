@@ -78,6 +78,20 @@ struct PrefillArgs {
   float scale_log2;
 };
 
+// Rows of a list of slots moved between the pool and a dense [n][Hkv][D]
+// buffer (gather: pool -> dense, scatter: dense -> pool).
+struct KvMoveArgs {
+  void* k_pool;           // gather source / scatter destination (only read by the gather)
+  void* v_pool;
+  void* k_dense;          // gather destination / scatter source (only read by the scatter)
+  void* v_dense;
+  const int32_t* slot_ids;
+  int32_t num_slots;
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t row_bytes;      // head_dim * element bytes (a multiple of 16)
+};
+
 // Decode planning shared by the launcher and the workspace query.
 struct DecodePlan {
   int32_t split_blocks;
@@ -90,6 +104,7 @@ size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max
 void set_decode_workspace(DecodeArgs& a, void* ws, bool bf16);
 
 hipError_t launch_kv_write(const KvWriteArgs& a, bool bf16, hipStream_t stream);
+hipError_t launch_kv_move(const KvMoveArgs& a, bool gather, hipStream_t stream);
 hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream);
 // Longest context the matrix-core prefill handles (its block table is staged
 // whole in LDS); longer contexts take the vector path.

@@ -61,3 +61,22 @@ extern "C" int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_
   }
   return bros::ok();
 }
+
+// A scatter's slot list: ids inside the pool must be distinct, else two rows
+// race for one slot.
+extern "C" int bros_check_slot_ids(const int32_t* slot_ids, int32_t num_slots, int32_t num_blocks) {
+  if (num_slots < 0 || num_blocks <= 0)
+    return fail(BROS_E_SHAPE, "bad counts: num_slots=%d num_blocks=%d", num_slots, num_blocks);
+  if (num_slots == 0) return bros::ok();
+  if (!slot_ids) return fail(BROS_E_NULL, "slot_ids is NULL");
+  const int64_t pool_slots = (int64_t)num_blocks * 16;
+  std::vector<uint8_t> seen((size_t)pool_slots, 0);
+  for (int32_t i = 0; i < num_slots; ++i) {
+    const int64_t id = slot_ids[i];
+    if (id < 0 || id >= pool_slots) continue;
+    if (seen[(size_t)id]) return fail(BROS_E_TABLE, "slot id %lld (block %lld slot %lld) appears again at index %d",
+                                      (long long)id, (long long)(id / 16), (long long)(id % 16), i);
+    seen[(size_t)id] = 1;
+  }
+  return bros::ok();
+}

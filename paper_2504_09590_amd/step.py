@@ -15,6 +15,18 @@ the decode, so the matrix-core bound and the HBM bound halves share the chip.
 With prefill_cus=N the two halves also get disjoint compute units: the
 prefill runs on a stream limited to the first N compute units, the write and
 the decode on a stream limited to the rest (N a multiple of 32).
+
+With swap_slots=N every step also checkpoints N slots and restores N slots
+(Sec. 5.2) through a SwapLane: the gather before the write, the scatter
+before the attention, the host copies on their own stream beside it. With
+copy_cus=C (a multiple of 32) that copy stream runs on the first C compute
+units and the rest of the step on the others, for a runtime that performs
+host copies as kernels. With swap_serial=True the copies go on the step's own
+stream between its kernels instead. The
+slots are early positions of decode sequences, which no write of the step
+touches, and the restore puts back the bytes they hold, so the step's outputs
+do not change; the step then waits for the copies, so its time is about
+max(t_exec, t_swap).
 """
 
 from __future__ import annotations
@@ -23,10 +35,12 @@ import numpy as np
 import torch
 
 from . import bros
+from .swap import SwapLane
 
 
 class MixedStep:
-    def __init__(self, batch, dev: bros.DeviceBatch, overlap: bool = False, prefill_cus: int = 0):
+    def __init__(self, batch, dev: bros.DeviceBatch, overlap: bool = False, prefill_cus: int = 0,
+                 swap_slots: int = 0, copy_cus: int = 0, swap_serial: bool = False):
         self.batch = batch
         self.dev = dev
         P, S = batch.num_prefill, batch.num_seqs
@@ -47,6 +61,14 @@ class MixedStep:
         self.prefill_cus = int(prefill_cus) if P > 0 and S > P else 0
         self.overlap = (overlap or self.prefill_cus > 0) and P > 0 and S > P
         self.main = None   # None: the caller's current stream
+        self.copy_cus = int(copy_cus) if swap_slots > 0 else 0
+        if self.copy_cus and self.prefill_cus:
+            raise ValueError("copy_cus and prefill_cus cannot be combined")
+        self._copy_stream = None
+        if self.copy_cus:
+            total = torch.cuda.get_device_properties(device).multi_processor_count
+            self._copy_stream = bros.bros_stream_create_cu_share(0, self.copy_cus)
+            self.main = bros.bros_stream_create_cu_share(self.copy_cus, total - self.copy_cus)
         if self.prefill_cus:
             total = torch.cuda.get_device_properties(device).multi_processor_count
             self.side = bros.bros_stream_create_cu_share(0, self.prefill_cus)
@@ -57,14 +79,65 @@ class MixedStep:
         self._ev_prefilled = torch.cuda.Event() if self.overlap else None
         self._ev_enter = torch.cuda.Event()
         self._ev_leave = torch.cuda.Event()
+        self.swap = None
+        self.swap_serial = bool(swap_serial)
+        if swap_slots > 0:
+            self._init_swap(int(swap_slots))
+
+    def _init_swap(self, n: int):
+        b, d = self.batch, self.dev
+        ids = []
+        for depth in range(int(b.ctx_lens.max())):
+            for s in range(self.P, self.S):
+                if depth < int(b.ctx_lens[s]) - 1 and len(ids) < n:
+                    # slot of logical position `depth` (Sec. 5.1: RT from the left, BE from the right)
+                    off = depth % 16
+                    slot = off if int(b.dir[s]) > 0 else 15 - off
+                    ids.append(int(b.block_tables[s][depth // 16]) * 16 + slot)
+            if len(ids) >= n:
+                break
+        if len(ids) < n:
+            raise ValueError(f"the batch's decode sequences hold fewer than {n} untouched slots")
+        ids = np.asarray(ids, dtype=np.int32)
+        bros.bros_check_slot_ids(ids, b.num_blocks)
+        self.swap_ids = torch.from_numpy(ids).to(d.k_pool.device)
+        hkv, hd = d.k_pool.shape[1], d.k_pool.shape[3]
+        self.swap = SwapLane(n, hkv, hd, d.k_pool.dtype, d.k_pool.device, copy_stream=self._copy_stream,
+                             serial=self.swap_serial)
+        pin = dict(dtype=d.k_pool.dtype, pin_memory=True)
+        self.host_out_k, self.host_out_v = torch.empty((n, hkv, hd), **pin), torch.empty((n, hkv, hd), **pin)
+        self.host_in_k, self.host_in_v = torch.empty((n, hkv, hd), **pin), torch.empty((n, hkv, hd), **pin)
+        # the rows the restore puts back: what the slots hold now
+        tk = torch.empty((n, hkv, hd), dtype=d.k_pool.dtype, device=d.k_pool.device)
+        tv = torch.empty_like(tk)
+        bros.bros_kv_gather(d.k_pool, d.v_pool, self.swap_ids, tk, tv)
+        torch.cuda.synchronize()
+        self.host_in_k.copy_(tk)
+        self.host_in_v.copy_(tv)
+        self.swap.prefetch(self.host_in_k, self.host_in_v, n)
+
+    # lazy checkpointing around the write ----------------------------------------
+    def swap_out(self, stream):
+        self.swap.checkpoint(self.dev.k_pool, self.dev.v_pool, self.swap_ids, self.host_out_k, self.host_out_v,
+                             stream)
+
+    def swap_in(self, stream):
+        self.swap.restore(self.swap_ids, self.dev.k_pool, self.dev.v_pool, stream)
+
+    def swap_next(self, stream):
+        """Prefetch for the next step's restore, then make `stream` wait for
+        every copy of this step."""
+        self.swap.prefetch(self.host_in_k, self.host_in_v, int(self.swap_ids.numel()), stream=stream)
+        self.swap.join(stream)
 
     def close(self):
         """Releases the compute-unit share streams (after their work is done)."""
-        if self.prefill_cus and self.main is not None:
+        if (self.prefill_cus or self.copy_cus) and self.main is not None:
             torch.cuda.synchronize()
-            bros.bros_stream_destroy(self.side)
-            bros.bros_stream_destroy(self.main)
-            self.main = self.side = None
+            for st in (self.side if self.prefill_cus else None, self._copy_stream, self.main):
+                if st is not None:
+                    bros.bros_stream_destroy(st)
+            self.main = self.side = self._copy_stream = None
 
     # the three calls --------------------------------------------------------
     def kv_write(self, stream=None):
@@ -96,8 +169,12 @@ class MixedStep:
         if main is not cur:
             self._ev_enter.record(cur)
             main.wait_event(self._ev_enter)
+        if self.swap is not None:
+            self.swap_out(main)
         if write:
             self.kv_write(main)
+        if self.swap is not None:
+            self.swap_in(main)
         if self.overlap:
             self._ev_written.record(main)
             self.side.wait_event(self._ev_written)
@@ -108,6 +185,8 @@ class MixedStep:
         else:
             self.prefill(main)
             self.decode(main)
+        if self.swap is not None:
+            self.swap_next(main)
         if main is not cur:
             self._ev_leave.record(main)
             cur.wait_event(self._ev_leave)

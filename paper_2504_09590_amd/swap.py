@@ -1,0 +1,131 @@
+"""Lazy checkpointing of shared blocks over two copy streams (Sec. 5.2, Sec. 6).
+
+When a write is about to take slots that still hold a peer request's tokens,
+only those tokens are saved to CPU memory, and they come back when the peer
+is scheduled again. On this device the two halves of that are different kinds
+of work. The gather and scatter over scattered 256-byte rows are HBM-bound
+and take microseconds (bros_kv_gather / bros_kv_scatter). The host copies are
+bound by the host link and belong on a copy engine (bros_copy_dma): a copy
+made as a kernel would take compute units from the attention or queue behind
+it. So a SwapLane gathers into a dense device staging buffer on the compute
+stream, copies it to pinned host memory on a copy stream, copies restored
+rows into a second staging buffer on the same copy stream ahead of time, and
+scatters them on the compute stream before the attention that reads them.
+One copy stream carries both directions in turn: on MI355X two copies in
+opposite directions at once each fall to about a third of their rate alone.
+Whether a host copy runs on a copy engine is the HIP runtime's choice: the
+runtime that ships with ROCm 7.2 honours the request, the one bundled with
+PyTorch for ROCm 7.0 performs such copies as kernels. A copy kernel needs
+compute units, so the copy stream can be given a compute-unit share of its
+own (bros_stream_create_cu_share) and the attention the rest; otherwise the
+copies queue behind a decode grid that fills every unit.
+The iteration then costs about max(t_exec, t_swap), as in the paper's cost
+model (Sec. 4.1).
+
+Ordering, all on the device (no host synchronisation):
+  checkpoint: compute stream  [waits: previous copy-out done] gather -> event
+              copy stream     [waits: gather] staging -> pinned host -> event
+  prefetch:   copy stream     [waits: previous scatter done] pinned host -> staging -> event
+  restore:    compute stream  [waits: prefetch] scatter -> event
+"""
+
+from __future__ import annotations
+
+import torch
+
+from . import bros
+
+
+class SwapLane:
+    def __init__(self, max_slots: int, num_kv_heads: int, head_dim: int, dtype: torch.dtype, device="cuda",
+                 copy_stream=None, serial: bool = False):
+        """serial=True enqueues the host copies on the compute stream itself,
+        between the kernels, instead of on a copy stream beside them."""
+        shape = (max(int(max_slots), 1), num_kv_heads, head_dim)
+        self.max_slots = int(max_slots)
+        self.out_k = torch.empty(shape, dtype=dtype, device=device)
+        self.out_v = torch.empty(shape, dtype=dtype, device=device)
+        self.in_k = torch.empty(shape, dtype=dtype, device=device)
+        self.in_v = torch.empty(shape, dtype=dtype, device=device)
+        self.serial = bool(serial)
+        self.copy = None if self.serial else (copy_stream if copy_stream is not None else torch.cuda.Stream(device=device))
+        self._gathered = torch.cuda.Event()
+        self._copied_out = torch.cuda.Event()
+        self._copied_in = torch.cuda.Event()
+        self._scattered = torch.cuda.Event()
+        self._copy_done = torch.cuda.Event()
+        self._out_pending = False
+        self._in_pending = False
+        self._n_in = 0
+        self.timing = None   # a list to collect ("d2h" | "h2d", start, end) timing events of every copy
+
+    def _mark(self, kind: str, cs):
+        if self.timing is None:
+            return None
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(cs)
+        self.timing.append((kind, a, b))
+        return b
+
+    def _close(self, end, cs) -> None:
+        if end is not None:
+            end.record(cs)
+
+    def _bytes(self, n: int) -> int:
+        return n * self.out_k[0].numel() * self.out_k.element_size()
+
+    def _room(self, n: int) -> None:
+        if n > self.max_slots:
+            raise ValueError(f"{n} slots exceed the lane's {self.max_slots}")
+
+    def checkpoint(self, k_pool, v_pool, slot_ids, host_k, host_v, stream) -> None:
+        """Saves the rows at slot_ids (device int32) to host_k/host_v (pinned,
+        [>= n][Hkv][D]). Enqueue it before the write that overwrites them."""
+        n = int(slot_ids.numel())
+        self._room(n)
+        if self._out_pending:
+            stream.wait_event(self._copied_out)        # the staging buffer is being copied out
+        bros.bros_kv_gather(k_pool, v_pool, slot_ids, self.out_k, self.out_v, num_slots=n, stream=stream)
+        self._gathered.record(stream)
+        cs = stream if self.serial else self.copy
+        cs.wait_event(self._gathered)
+        t = self._mark("d2h", cs)
+        bros.bros_copy_dma(host_k, self.out_k, self._bytes(n), stream=cs)
+        bros.bros_copy_dma(host_v, self.out_v, self._bytes(n), stream=cs)
+        self._copied_out.record(cs)
+        self._close(t, cs)
+        self._out_pending = True
+
+    def prefetch(self, host_k, host_v, n: int, stream=None) -> None:
+        """Starts copying n checkpointed rows back to the device (on `stream`
+        in serial mode, else on the copy stream)."""
+        self._room(n)
+        cs = self.copy
+        if self.serial:
+            cs = stream if stream is not None else torch.cuda.current_stream()
+        if self._in_pending:
+            cs.wait_event(self._scattered)             # the previous restore still reads the buffer
+        t = self._mark("h2d", cs)
+        bros.bros_copy_dma(self.in_k, host_k, self._bytes(n), stream=cs)
+        bros.bros_copy_dma(self.in_v, host_v, self._bytes(n), stream=cs)
+        self._copied_in.record(cs)
+        self._close(t, cs)
+        self._n_in = n
+
+    def restore(self, slot_ids, k_pool, v_pool, stream) -> None:
+        """Scatters the prefetched rows to slot_ids (device int32, as many as
+        were prefetched). Enqueue it before the attention that reads them."""
+        n = int(slot_ids.numel())
+        if n != self._n_in:
+            raise ValueError(f"restore of {n} slots after a prefetch of {self._n_in}")
+        stream.wait_event(self._copied_in)
+        bros.bros_kv_scatter(self.in_k, self.in_v, slot_ids, k_pool, v_pool, num_slots=n, stream=stream)
+        self._scattered.record(stream)
+        self._in_pending = True
+
+    def join(self, stream) -> None:
+        """Makes `stream` wait for every copy enqueued so far."""
+        if self.serial:
+            return
+        self._copy_done.record(self.copy)
+        stream.wait_event(self._copy_done)

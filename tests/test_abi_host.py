@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings_and_version():
     for code, name in bros.STATUS.items():
         assert bros.LIB.bros_status_str(code).decode() == name
-    assert bros.LIB.bros_abi_version() == 2
+    assert bros.LIB.bros_abi_version() == 4
 
 
 # --- argument validation (returns before any HIP call) -----------------------
@@ -108,6 +108,42 @@ def test_prefill_rejects():
     assert L.bros_attn_prefill_chunk(*a) == -5
     a = list(base); a[3] = 0
     assert L.bros_attn_prefill_chunk(*a) == 0
+
+
+@pytest.mark.parametrize("fn", ["bros_kv_gather", "bros_kv_scatter"])
+def test_kv_move_rejects(fn):
+    L = getattr(bros.LIB, fn)
+    if fn == "bros_kv_gather":   # k_pool, v_pool, nb, ids, n, k_out, v_out, hkv, d, bs, dtype, stream
+        base = [FAKE, FAKE, 10, FAKE, 5, FAKE, FAKE, 8, 128, 16, 1, None]
+        idx = dict(nb=2, ids=3, n=4, hkv=7, d=8, bs=9, dtype=10, ptr=5)
+    else:                        # k_in, v_in, ids, n, k_pool, v_pool, nb, hkv, d, bs, dtype, stream
+        base = [FAKE, FAKE, FAKE, 5, FAKE, FAKE, 10, 8, 128, 16, 1, None]
+        idx = dict(nb=6, ids=2, n=3, hkv=7, d=8, bs=9, dtype=10, ptr=0)
+    for key, val, code in (("dtype", 7, -3), ("bs", 8, -4), ("d", 64, -4), ("hkv", 0, -2), ("n", -1, -2),
+                           ("nb", 0, -2), ("ids", None, -1), ("ptr", None, -1), ("ptr", FAKE + 4, -2)):
+        a = list(base)
+        a[idx[key]] = val
+        assert L(*a) == code, (key, val)
+    a = list(base)
+    a[idx["n"]] = 0
+    a[idx["ids"]] = None
+    assert L(*a) == 0               # nothing to move: no-op
+
+
+def test_copy_dma_rejects_null_and_allows_empty():
+    assert bros.LIB.bros_copy_dma(None, FAKE, 16, None) == -1
+    assert bros.LIB.bros_copy_dma(FAKE, None, 16, None) == -1
+    assert bros.LIB.bros_copy_dma(None, None, 0, None) == 0
+
+
+def test_check_slot_ids():
+    ok = np.array([5, 3, 159, -1, -1, 160, 160, 0], dtype=np.int32)   # repeats only outside the pool
+    bros.bros_check_slot_ids(ok, 10)
+    with pytest.raises(bros.BrosError, match="slot id 3"):
+        bros.bros_check_slot_ids(np.array([1, 3, 2, 3], dtype=np.int32), 10)
+    assert bros.LIB.bros_check_slot_ids(None, 0, 10) == 0
+    assert bros.LIB.bros_check_slot_ids(None, 2, 10) == -1
+    assert bros.LIB.bros_check_slot_ids(None, 2, 0) == -2
 
 
 @pytest.mark.parametrize("first,num", [(0, 0), (0, 48), (16, 32), (-32, 64), (0, -32)])

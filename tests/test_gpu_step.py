@@ -7,6 +7,7 @@ grid fits a share)."""
 import numpy as np
 import pytest
 
+import oracle
 from paper_2504_09590_amd import workload as W
 from tests.gpu_helpers import announce, compare, oracle_step, require_gpu
 
@@ -19,17 +20,29 @@ def mixed():
     return b, oracle_step(b)
 
 
-@pytest.mark.parametrize("overlap,prefill_cus", [(False, 0), (True, 0), (True, 64), (True, 224)])
-def test_mixed_step_full(mixed, overlap, prefill_cus):
+@pytest.mark.parametrize("overlap,prefill_cus,swap_slots,copy_cus",
+                         [(False, 0, 0, 0), (True, 0, 0, 0), (True, 64, 0, 0), (True, 224, 0, 0), (False, 0, 1024, 0),
+                          (True, 0, 1024, 32), (False, 0, -1024, 0)])
+def test_mixed_step_full(mixed, overlap, prefill_cus, swap_slots, copy_cus):
+    serial = swap_slots < 0          # a negative count: the serial arrangement
+    swap_slots = abs(swap_slots)
     torch = require_gpu()
     from paper_2504_09590_amd import bros
     from paper_2504_09590_amd.step import MixedStep
     b, (k1, v1, pre_ref, dec_ref) = mixed
     dev = bros.to_device(b)
-    announce(f"mixed step {b.name} overlap={overlap} prefill_cus={prefill_cus}")
-    step = MixedStep(b, dev, overlap=overlap, prefill_cus=prefill_cus)
+    announce(f"mixed step {b.name} overlap={overlap} prefill_cus={prefill_cus} swap_slots={swap_slots} "
+             f"copy_cus={copy_cus} serial={serial}")
+    step = MixedStep(b, dev, overlap=overlap, prefill_cus=prefill_cus, swap_slots=swap_slots, copy_cus=copy_cus,
+                     swap_serial=serial)
     pre, dec = step.run()
+    if swap_slots:   # a second step restores what the first checkpointed
+        pre, dec = step.run()
     torch.cuda.synchronize()
+    if swap_slots:
+        ids = step.swap_ids.cpu().numpy()
+        assert np.array_equal(bros.to_host_bits(step.host_out_k), oracle.kv_gather(k1, ids))
+        assert np.array_equal(bros.to_host_bits(step.host_out_v), oracle.kv_gather(v1, ids))
     step.close()
     for name, ref, got in (("k", k1, dev.k_pool), ("v", v1, dev.v_pool)):
         assert np.array_equal(bros.to_host_bits(got), ref), f"{name} pool after the step"
