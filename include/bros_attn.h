@@ -36,6 +36,10 @@
  *   dir:          int8 [num_seqs], +1 (left-to-right) or -1 (right-to-left).
  *                 May be NULL: then the direction is derived from cls
  *                 (RT -> +1, BE -> -1), which is the layout of Sec. 5.1.
+ *   dir_per_entry: 0 for the form above; 1 when dir is the paper's
+ *                 direction table (Sec. 6), int8 [num_seqs][max_blocks_per_seq]
+ *                 with one flag per block-table entry: positions of entry i
+ *                 are walked in that entry's direction. Requires dir.
  *   cls:          uint8 [num_seqs], BROS_RT or BROS_BE. Only consulted when
  *                 dir is NULL; it has no other numerical effect. May be NULL
  *                 when dir is given.
@@ -112,7 +116,7 @@ int bros_abi_version(void);
 int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
                   void* k_pool, void* v_pool, int32_t num_blocks,
                   const int32_t* block_tables, int32_t max_blocks_per_seq,
-                  const int8_t* dir, const uint8_t* cls,
+                  const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry,
                   const int32_t* pos0, const int32_t* cu_new,
                   int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
                   int32_t block_size, int32_t dtype, void* stream);
@@ -149,7 +153,7 @@ int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
 int bros_attn_decode(void* out, const void* q,
                      const void* k_pool, const void* v_pool, int32_t num_blocks,
                      const int32_t* block_tables, int32_t max_blocks_per_seq,
-                     const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                     const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
                      int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
                      int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                      float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
@@ -181,7 +185,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
                             int32_t num_q_tokens, int32_t max_q_len,
                             const void* k_pool, const void* v_pool, int32_t num_blocks,
                             const int32_t* block_tables, int32_t max_blocks_per_seq,
-                            const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                            const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
                             int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
                             int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                             float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
@@ -298,15 +302,16 @@ int bros_stream_destroy(void* stream);
  * own the same slot; a peer's token that would be overwritten is checkpointed
  * first, so a consistent batch maps distinct (sequence, position) pairs to
  * distinct (block, slot) pairs). All pointers are HOST pointers. Checks, in
- * order: counts and pointers, dir values in {+1, -1} (or cls in {RT, BE} when
- * dir is NULL), 0 <= ctx_lens[s] <= max_blocks_per_seq * 16, every referenced
+ * order: counts and pointers, dir values in {+1, -1} (per sequence, or per
+ * table entry below ceil(ctx / 16) when dir_per_entry is 1; cls in {RT, BE}
+ * when dir is NULL), 0 <= ctx_lens[s] <= max_blocks_per_seq * 16, every referenced
  * table entry in [0, num_blocks), and -- when check_slot_disjointness != 0 --
  * that no (block, slot) is owned twice. Returns BROS_OK or BROS_E_TABLE (or
  * BROS_E_NULL / BROS_E_SHAPE / BROS_E_UNSUPPORTED) with a message naming the
  * first offending sequence and position.
  */
 int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_per_seq,
-                     const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                     const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
                      int32_t num_seqs, int32_t num_blocks, int32_t block_size,
                      int32_t check_slot_disjointness);
 

@@ -49,15 +49,15 @@ def _load() -> ctypes.CDLL:
     lib.bros_last_error.restype = ctypes.c_char_p
     lib.bros_abi_version.argtypes = []
     lib.bros_abi_version.restype = ctypes.c_int
-    lib.bros_kv_write.argtypes = [P, P, I, P, P, I, P, I, P, P, P, P, I, I, I, I, I, P]
+    lib.bros_kv_write.argtypes = [P, P, I, P, P, I, P, I, P, P, I, P, P, I, I, I, I, I, P]
     lib.bros_kv_write.restype = ctypes.c_int
-    lib.bros_attn_decode.argtypes = [P, P, P, P, I, P, I, P, P, P, I, I, I, I, I, I, F, I, P, Z, P]
+    lib.bros_attn_decode.argtypes = [P, P, P, P, I, P, I, P, P, I, P, I, I, I, I, I, I, F, I, P, Z, P]
     lib.bros_attn_decode.restype = ctypes.c_int
-    lib.bros_attn_prefill_chunk.argtypes = [P, P, P, I, I, P, P, I, P, I, P, P, P, I, I, I, I, I, I, F, I, P, Z, P]
+    lib.bros_attn_prefill_chunk.argtypes = [P, P, P, I, I, P, P, I, P, I, P, P, I, P, I, I, I, I, I, I, F, I, P, Z, P]
     lib.bros_attn_prefill_chunk.restype = ctypes.c_int
     lib.bros_attn_workspace_size.argtypes = [I, I, I, I, I, I]
     lib.bros_attn_workspace_size.restype = Z
-    lib.bros_check_batch.argtypes = [P, I, P, P, P, I, I, I, I]
+    lib.bros_check_batch.argtypes = [P, I, P, P, I, P, I, I, I, I]
     lib.bros_check_batch.restype = ctypes.c_int
     lib.bros_stream_create_cu_share.argtypes = [I, I, ctypes.POINTER(ctypes.c_void_p)]
     lib.bros_stream_create_cu_share.restype = ctypes.c_int
@@ -115,12 +115,22 @@ def _numel0(t) -> int:
     return 0 if t is None else int(t.shape[0])
 
 
+def _dir_mode(dir, block_tables) -> int:
+    """0 for one flag per sequence, 1 for the direction table (one flag per
+    block-table entry, shaped like the tables)."""
+    if dir is None or len(dir.shape) == 1:
+        return 0
+    if tuple(dir.shape) != tuple(block_tables.shape):
+        raise ValueError(f"direction table {tuple(dir.shape)} must match block tables {tuple(block_tables.shape)}")
+    return 1
+
+
 def bros_kv_write(k_new, v_new, k_pool, v_pool, block_tables, dir, cls, pos0, cu_new, stream=None):
     """Store new tokens' K/V ([Tn][Hkv][D]) in their bidirectional slots of the pools."""
     nb, hkv, bs, d = (int(x) for x in k_pool.shape)
     _check(LIB.bros_kv_write(_ptr(k_new), _ptr(v_new), _numel0(k_new), _ptr(k_pool), _ptr(v_pool), nb,
                              _ptr(block_tables), int(block_tables.shape[1]), _ptr(dir), _ptr(cls),
-                             _ptr(pos0), _ptr(cu_new), int(cu_new.shape[0]) - 1, hkv, d, bs,
+                             _dir_mode(dir, block_tables), _ptr(pos0), _ptr(cu_new), int(cu_new.shape[0]) - 1, hkv, d, bs,
                              _dtype_code(k_pool), _stream(stream)))
 
 
@@ -135,8 +145,8 @@ def bros_attn_decode(out, q, k_pool, v_pool, block_tables, dir, cls, ctx_lens, m
     nb, hkv, bs, d = (int(x) for x in k_pool.shape)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(LIB.bros_attn_decode(_ptr(out), _ptr(q), _ptr(k_pool), _ptr(v_pool), nb, _ptr(block_tables),
-                                int(block_tables.shape[1]), _ptr(dir), _ptr(cls), _ptr(ctx_lens),
-                                int(max_ctx), int(ctx_lens.shape[0]), int(q.shape[1]), hkv, d, bs,
+                                int(block_tables.shape[1]), _ptr(dir), _ptr(cls), _dir_mode(dir, block_tables),
+                                _ptr(ctx_lens), int(max_ctx), int(ctx_lens.shape[0]), int(q.shape[1]), hkv, d, bs,
                                 float(scale), _dtype_code(q), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
@@ -147,8 +157,8 @@ def bros_attn_prefill_chunk(out, q, cu_q, max_q_len: int, k_pool, v_pool, block_
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(LIB.bros_attn_prefill_chunk(_ptr(out), _ptr(q), _ptr(cu_q), int(q.shape[0]), int(max_q_len),
                                        _ptr(k_pool), _ptr(v_pool), nb, _ptr(block_tables),
-                                       int(block_tables.shape[1]), _ptr(dir), _ptr(cls), _ptr(ctx_lens),
-                                       int(max_ctx), int(ctx_lens.shape[0]), int(q.shape[1]), hkv, d, bs,
+                                       int(block_tables.shape[1]), _ptr(dir), _ptr(cls),
+                                       _dir_mode(dir, block_tables), _ptr(ctx_lens), int(max_ctx), int(ctx_lens.shape[0]), int(q.shape[1]), hkv, d, bs,
                                        float(scale), _dtype_code(q), _ptr(workspace), ws_bytes,
                                        _stream(stream)))
 
@@ -161,7 +171,7 @@ def bros_check_batch(block_tables: np.ndarray, dir, cls, ctx_lens: np.ndarray, n
     dr = None if dir is None else np.ascontiguousarray(dir, dtype=np.int8)
     cs = None if cls is None else np.ascontiguousarray(cls, dtype=np.uint8)
     _check(LIB.bros_check_batch(_ptr(bt), int(bt.shape[1]) if bt.ndim == 2 else 0, _ptr(dr), _ptr(cs),
-                                _ptr(cl), int(cl.shape[0]), int(num_blocks), int(block_size),
+                                _dir_mode(dr, bt), _ptr(cl), int(cl.shape[0]), int(num_blocks), int(block_size),
                                 1 if check_slot_disjointness else 0))
 
 

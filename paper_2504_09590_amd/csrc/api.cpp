@@ -32,9 +32,11 @@ int check_shapes(const char* fn, int32_t num_q_heads, int32_t num_kv_heads, int3
 }
 
 int check_meta(const char* fn, const void* block_tables, int32_t max_blocks_per_seq, const int8_t* dir,
-               const uint8_t* cls, int32_t num_blocks) {
+               const uint8_t* cls, int32_t dir_per_entry, int32_t num_blocks) {
   if (block_tables == nullptr) return fail(BROS_E_NULL, "%s: block_tables is NULL", fn);
   if (dir == nullptr && cls == nullptr) return fail(BROS_E_NULL, "%s: dir and cls are both NULL", fn);
+  if (dir_per_entry != 0 && dir_per_entry != 1) return fail(BROS_E_SHAPE, "%s: dir_per_entry %d is neither 0 nor 1", fn, dir_per_entry);
+  if (dir_per_entry && dir == nullptr) return fail(BROS_E_NULL, "%s: dir_per_entry is set but dir is NULL", fn);
   if (max_blocks_per_seq <= 0) return fail(BROS_E_SHAPE, "%s: max_blocks_per_seq %d must be positive", fn, max_blocks_per_seq);
   if (num_blocks <= 0) return fail(BROS_E_SHAPE, "%s: num_blocks %d must be positive", fn, num_blocks);
   if (!aligned(block_tables, 4)) return fail(BROS_E_SHAPE, "%s: block_tables is not 4-byte aligned", fn);
@@ -61,7 +63,7 @@ extern "C" {
 int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
                   void* k_pool, void* v_pool, int32_t num_blocks,
                   const int32_t* block_tables, int32_t max_blocks_per_seq,
-                  const int8_t* dir, const uint8_t* cls,
+                  const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry,
                   const int32_t* pos0, const int32_t* cu_new,
                   int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
                   int32_t block_size, int32_t dtype, void* stream) {
@@ -73,11 +75,11 @@ int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
   if (num_new_tokens == 0) return ok();
   if (num_seqs == 0) return fail(BROS_E_SHAPE, "%s: %d new tokens but no sequences", fn, num_new_tokens);
   if (!k_new || !v_new || !k_pool || !v_pool || !pos0 || !cu_new) return fail(BROS_E_NULL, "%s: a tensor or offset pointer is NULL", fn);
-  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, num_blocks);
+  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, dir_per_entry, num_blocks);
   if (st) return st;
   if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16))
     return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
-  bros::KvWriteArgs a{k_new, v_new, k_pool, v_pool, block_tables, dir, cls, pos0, cu_new,
+  bros::KvWriteArgs a{k_new, v_new, k_pool, v_pool, block_tables, dir, cls, pos0, cu_new, dir_per_entry,
                       num_new_tokens, num_seqs, num_blocks, max_blocks_per_seq, num_kv_heads};
   return launch_status(fn, bros::launch_kv_write(a, dtype == BROS_BF16, static_cast<hipStream_t>(stream)));
 }
@@ -96,7 +98,7 @@ size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
 int bros_attn_decode(void* out, const void* q,
                      const void* k_pool, const void* v_pool, int32_t num_blocks,
                      const int32_t* block_tables, int32_t max_blocks_per_seq,
-                     const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                     const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
                      int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
                      int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                      float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
@@ -108,7 +110,7 @@ int bros_attn_decode(void* out, const void* q,
   if (num_seqs < 0 || max_ctx < 0) return fail(BROS_E_SHAPE, "%s: negative count (seqs=%d max_ctx=%d)", fn, num_seqs, max_ctx);
   if (num_seqs == 0) return ok();
   if (!out || !q || !k_pool || !v_pool || !ctx_lens) return fail(BROS_E_NULL, "%s: a tensor or length pointer is NULL", fn);
-  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, num_blocks);
+  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, dir_per_entry, num_blocks);
   if (st) return st;
   if (!aligned(out, 16) || !aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16))
     return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
@@ -127,6 +129,7 @@ int bros_attn_decode(void* out, const void* q,
   a.block_tables = block_tables;
   a.dir = dir;
   a.cls = cls;
+  a.dir_per_entry = dir_per_entry;
   a.ctx_lens = ctx_lens;
   a.cu_q = nullptr;
   a.num_rows = num_seqs;
@@ -147,7 +150,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
                             int32_t num_q_tokens, int32_t max_q_len,
                             const void* k_pool, const void* v_pool, int32_t num_blocks,
                             const int32_t* block_tables, int32_t max_blocks_per_seq,
-                            const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                            const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
                             int32_t max_ctx, int32_t num_seqs, int32_t num_q_heads,
                             int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                             float scale, int32_t dtype, void* workspace, size_t workspace_bytes,
@@ -161,7 +164,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   if (num_seqs == 0 || num_q_tokens == 0) return ok();
   if (max_q_len == 0) return fail(BROS_E_SHAPE, "%s: max_q_len is 0 with %d query rows", fn, num_q_tokens);
   if (!out || !q || !cu_q || !k_pool || !v_pool || !ctx_lens) return fail(BROS_E_NULL, "%s: a tensor or length pointer is NULL", fn);
-  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, num_blocks);
+  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, dir_per_entry, num_blocks);
   if (st) return st;
   if (!aligned(out, 16) || !aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16))
     return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
@@ -178,6 +181,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
     a.block_tables = block_tables;
     a.dir = dir;
     a.cls = cls;
+  a.dir_per_entry = dir_per_entry;
     a.ctx_lens = ctx_lens;
     a.num_q_tokens = num_q_tokens;
     a.num_seqs = num_seqs;
@@ -211,6 +215,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   a.block_tables = block_tables;
   a.dir = dir;
   a.cls = cls;
+  a.dir_per_entry = dir_per_entry;
   a.ctx_lens = ctx_lens;
   a.cu_q = cu_q;
   a.num_rows = num_q_tokens;

@@ -23,6 +23,15 @@ __device__ __forceinline__ int seq_direction(const int8_t* dir, const uint8_t* c
   return cls[s] == 1 ? -1 : 1;
 }
 
+// Direction of block-table entry e of sequence s. With per_entry set, dir is
+// the paper's direction table, shaped like the block tables ([S][max_blocks],
+// Sec. 6); otherwise one flag per sequence (or the class when dir is NULL).
+__device__ __forceinline__ int entry_direction(const int8_t* dir, const uint8_t* cls, int per_entry,
+                                               int max_blocks, int s, int e) {
+  if (dir != nullptr && per_entry) return dir[(size_t)s * max_blocks + e] < 0 ? -1 : 1;
+  return seq_direction(dir, cls, s);
+}
+
 // bf16 <-> fp32. Widening is exact (a shift); narrowing rounds to nearest-even
 // and keeps NaNs quiet.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

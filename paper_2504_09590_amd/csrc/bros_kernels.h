@@ -17,6 +17,7 @@ struct KvWriteArgs {
   const uint8_t* cls;
   const int32_t* pos0;
   const int32_t* cu_new;
+  int32_t dir_per_entry;  // dir is [S][max_blocks_per_seq] (else [S])
   int32_t num_new_tokens;
   int32_t num_seqs;
   int32_t num_blocks;
@@ -38,6 +39,7 @@ struct DecodeArgs {
   const uint8_t* cls;
   const int32_t* ctx_lens;
   const int32_t* cu_q;
+  int32_t dir_per_entry;  // dir is [S][max_blocks_per_seq] (else [S])
   // Partial results. fp32 split-K: [rows][Hq][n_split_max] slots. bf16 (one
   // worker per wave over an even share of the tiles): slot (row * Hkv + g +
   // worker) * G + head-in-group, for segments cut between workers.
@@ -67,6 +69,7 @@ struct PrefillArgs {
   const int8_t* dir;
   const uint8_t* cls;
   const int32_t* ctx_lens;
+  int32_t dir_per_entry;  // dir is [S][max_blocks_per_seq] (else [S])
   int32_t num_q_tokens;
   int32_t num_seqs;
   int32_t num_blocks;

@@ -15,7 +15,7 @@
 using bros::fail;
 
 extern "C" int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_per_seq,
-                                const int8_t* dir, const uint8_t* cls, const int32_t* ctx_lens,
+                                const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
                                 int32_t num_seqs, int32_t num_blocks, int32_t block_size,
                                 int32_t check_slot_disjointness) {
   if (block_size != 16) return fail(BROS_E_UNSUPPORTED, "block_size %d unsupported (16 only)", block_size);
@@ -25,11 +25,20 @@ extern "C" int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_
   if (!block_tables || !ctx_lens) return fail(BROS_E_NULL, "block_tables or ctx_lens is NULL");
   if (!dir && !cls) return fail(BROS_E_NULL, "dir and cls are both NULL");
 
+  if (dir_per_entry != 0 && dir_per_entry != 1) return fail(BROS_E_SHAPE, "dir_per_entry %d is neither 0 nor 1", dir_per_entry);
+  if (dir_per_entry && !dir) return fail(BROS_E_NULL, "dir_per_entry is set but dir is NULL");
+  // Direction of table entry b of sequence s (validated below).
+  auto dir_of = [&](int s, int b) -> int {
+    if (!dir) return cls[s] == 1 ? -1 : 1;
+    return dir_per_entry ? dir[(size_t)s * max_blocks_per_seq + b] : dir[s];
+  };
   std::vector<int> d(num_seqs);
   for (int s = 0; s < num_seqs; ++s) {
-    if (dir) {
+    if (dir && !dir_per_entry) {
       if (dir[s] != 1 && dir[s] != -1) return fail(BROS_E_TABLE, "sequence %d: direction flag %d is not +1 or -1", s, (int)dir[s]);
       d[s] = dir[s];
+    } else if (dir) {
+      d[s] = 1;   // per entry: checked with the table below
     } else {
       if (cls[s] > 1) return fail(BROS_E_TABLE, "sequence %d: class %u is neither RT (0) nor BE (1)", s, (unsigned)cls[s]);
       d[s] = cls[s] == 1 ? -1 : 1;
@@ -42,6 +51,10 @@ extern "C" int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_
       const int32_t id = block_tables[(size_t)s * max_blocks_per_seq + b];
       if (id < 0 || id >= num_blocks)
         return fail(BROS_E_TABLE, "sequence %d: table entry %d = %d outside [0, %d)", s, b, id, num_blocks);
+      if (dir_per_entry) {
+        const int f = dir[(size_t)s * max_blocks_per_seq + b];
+        if (f != 1 && f != -1) return fail(BROS_E_TABLE, "sequence %d entry %d: direction flag %d is not +1 or -1", s, b, f);
+      }
     }
   }
   if (!check_slot_disjointness) return bros::ok();
@@ -52,7 +65,7 @@ extern "C" int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_
     for (int p = 0; p < ctx_lens[s]; ++p) {
       const int32_t id = block_tables[(size_t)s * max_blocks_per_seq + p / 16];
       const int off = p % 16;
-      const int slot = d[s] > 0 ? off : 15 - off;
+      const int slot = (dir_per_entry ? dir_of(s, p / 16) : d[s]) > 0 ? off : 15 - off;
       const uint16_t bit = (uint16_t)(1u << slot);
       if (used[id] & bit)
         return fail(BROS_E_TABLE, "sequence %d position %d: block %d slot %d is already owned by another token", s, p, id, slot);

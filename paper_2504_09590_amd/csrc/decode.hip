@@ -121,7 +121,8 @@ __device__ __forceinline__ void enter_row(const DecodeArgs& a, int row, Cursor& 
   c.row = row;
   resolve_row(a, row, c.s, c.ctx);
   c.nblk = c.ctx > 0 ? (c.ctx + kBlockSize - 1) / kBlockSize : 0;
-  c.dirv = seq_direction(a.dir, a.cls, c.s);
+  // Only the tail block has slots outside the context: its entry's direction.
+  c.dirv = entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, c.s, c.nblk > 0 ? c.nblk - 1 : 0);
   c.row = __builtin_amdgcn_readfirstlane(c.row);
   c.s = __builtin_amdgcn_readfirstlane(c.s);
   c.ctx = __builtin_amdgcn_readfirstlane(c.ctx);

@@ -308,7 +308,8 @@ __device__ __forceinline__ void fetch_item(const DecodeArgs& a, const int* s_pre
   it.b_begin = it.split * SB;
   const int nb = it.split < it.nsp ? max(0, min(it.nblk, it.b_begin + SB) - it.b_begin) : 0;
   it.nbw = nb > stream ? (nb - stream + NSTREAM - 1) / NSTREAM : 0;
-  it.dirv = seq_direction(a.dir, a.cls, it.s);
+  // Only the tail block has slots outside the context: its entry's direction.
+  it.dirv = entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, it.s, it.nblk > 0 ? it.nblk - 1 : 0);
   // Every field but the table entry is the same on all lanes: keep them in
   // scalar registers so the vector registers go to KV fragments.
   it.row = __builtin_amdgcn_readfirstlane(it.row);

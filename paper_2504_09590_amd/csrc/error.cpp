@@ -47,6 +47,6 @@ const char* bros_status_str(int status) {
 
 const char* bros_last_error(void) { return g_last_error.c_str(); }
 
-int bros_abi_version(void) { return 4; }
+int bros_abi_version(void) { return 5; }
 
 }  // extern "C"

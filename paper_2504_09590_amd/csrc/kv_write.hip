@@ -1,7 +1,8 @@
 // bros_kv_write on gfx950: store each new token's K/V rows in the slot its
-// sequence's direction assigns (RT from the left end of a block, BE from the
+// block's direction assigns (RT from the left end of a block, BE from the
 // right end; Sec. 5.1), with the exclusive view of Sec. 5.2 (entry i of a
-// sequence's table holds its positions [16 i, 16 i + 16)).
+// sequence's table holds its positions [16 i, 16 i + 16)). The direction is
+// the sequence's, or that of the token's table entry (Sec. 6's table).
 //
 // One workgroup moves kTokens tokens. Its 256 threads first request the
 // tokens' source rows (16-byte chunks), which do not depend on the
@@ -67,13 +68,13 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
   for (int j = tid; j < a.num_seqs; j += kThreads) {
     const int lo = a.cu_new[j], hi = a.cu_new[j + 1];
     const int p0 = a.pos0[j];
-    const int dirv = seq_direction(a.dir, a.cls, j);
     const int k0 = max(lo, t0), k1 = min(hi, min(t0 + kTokens, a.num_new_tokens));
     for (int k = k0; k < k1; ++k) {
       const int p = p0 + (k - lo);
       int dst = -1;
       if (p >= 0 && (p >> 4) < a.max_blocks_per_seq) {
         const int blk = a.block_tables[(size_t)j * a.max_blocks_per_seq + (p >> 4)];
+        const int dirv = entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, j, p >> 4);
         if (blk >= 0 && blk < a.num_blocks) dst = blk * kBlockSize + slot_of_offset(p & 15, dirv);
       }
       s_dst[k - t0] = dst;

@@ -155,6 +155,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   __shared__ __attribute__((aligned(1024))) uint8_t s_vring[kSlots * kSlotBytes];
   __shared__ int s_first_bad;
   __shared__ int s_tbl[kMaxTableLds];   // the sequence's validated table entries (-1: invalid)
+  __shared__ int8_t s_dir[kMaxTableLds];   // each entry's direction (+1 / -1)
   __shared__ __attribute__((aligned(16))) int s_len[kMaxRankItems];
   __shared__ int s_item;
 
@@ -223,7 +224,6 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   const int n_kt = (kend + kKeys - 1) / kKeys;   // key tiles of the unit
   if (n_kt == 0) return;
   const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
-  const int dirv = seq_direction(a.dir, a.cls, s);
   // keys below this logical position are visible to every row of the unit
   const int full_below = min(ctx, c0 + t0 + 1);
   const int n_steps = (n_kt + 1) / 2;        // both halves step together
@@ -303,6 +303,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     const int b = 2 * tile + my_bt;
     if (blk >= 0 && (b + 1) * kBlockSize <= ctx) return;
     uint8_t* dv = ring + kh * kTileBytes + 8 * rg * kRowBytes;
+    const int dirv = s_dir[b < nblk ? b : 0];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const int r8 = 4 * p + ld_slot;   // row among the wave's 8
@@ -365,10 +366,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
       const int lim = min(qpos, ctx - 1);
       const bool ok0 = (2 * tile < nblk ? s_tbl[2 * tile] : -1) >= 0;
       const bool ok1 = (2 * tile + 1 < nblk ? s_tbl[2 * tile + 1] : -1) >= 0;
+      const int dir0 = s_dir[2 * tile < nblk ? 2 * tile : 0];
+      const int dir1 = s_dir[2 * tile + 1 < nblk ? 2 * tile + 1 : 0];
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int k = 8 * (j >> 2) + 4 * half + (j & 3);   // j is a constant; half per lane
-        const int pos = 32 * tile + (k & 16) + slot_of_offset(k & 15, dirv);
+        const int pos = 32 * tile + (k & 16) + slot_of_offset(k & 15, (j >> 3) ? dir1 : dir0);
         const bool ok = (j >> 3) ? ok1 : ok0;   // k / 16 == j / 8
         cur[j] = (ok && pos <= lim) ? cur[j] : -INFINITY;
       }
@@ -495,6 +498,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     const int v = tbl[b];
     const bool ok = v >= 0 && v < a.num_blocks;
     s_tbl[b] = ok ? v : -1;
+    s_dir[b] = (int8_t)entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, s, b);
     if (!ok) atomicMin(&s_first_bad, b);
   }
   __syncthreads();

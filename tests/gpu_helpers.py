@@ -76,3 +76,20 @@ def oracle_step(batch, decode_seqs=None, prefill_seqs=None):
     dec = oracle.decode(batch.q_decode, k1, v1, batch.block_tables[P:], batch.dir[P:], batch.ctx_lens[P:],
                         batch.dtype, seqs=decode_seqs)
     return k1, v1, pre, dec
+
+
+def with_direction_table(batch, frac: float = 0.5, seed: int = 0):
+    """A copy of the batch whose `dir` is the paper's direction table (one flag
+    per block-table entry, Sec. 6): the per-sequence flags broadcast over the
+    row, then a random `frac` of the entries whose block the sequence fills
+    completely flipped. A full block has no peer, so the flipped batch stays
+    consistent; its slots are simply walked the other way."""
+    import dataclasses
+    rng = np.random.default_rng(seed)
+    maxb = batch.block_tables.shape[1]
+    tab = np.repeat(np.asarray(batch.dir, dtype=np.int8)[:, None], maxb, axis=1)
+    for s in range(batch.num_seqs):
+        full = int(batch.ctx_lens[s]) // 16
+        flip = np.nonzero(rng.random(full) < frac)[0]
+        tab[s, flip] = -tab[s, flip]
+    return dataclasses.replace(batch, dir=np.ascontiguousarray(tab))

@@ -43,18 +43,18 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings_and_version():
     for code, name in bros.STATUS.items():
         assert bros.LIB.bros_status_str(code).decode() == name
-    assert bros.LIB.bros_abi_version() == 4
+    assert bros.LIB.bros_abi_version() == 5
 
 
 # --- argument validation (returns before any HIP call) -----------------------
 
 def _decode(**kw):
-    args = dict(out=FAKE, q=FAKE, k=FAKE, v=FAKE, nb=10, bt=FAKE, maxb=4, dir=FAKE, cls=None,
+    args = dict(out=FAKE, q=FAKE, k=FAKE, v=FAKE, nb=10, bt=FAKE, maxb=4, dir=FAKE, cls=None, dpe=0,
                 ctx=FAKE, max_ctx=64, S=2, hq=8, hkv=2, d=128, bs=16, scale=0.0, dtype=1,
                 ws=None, wsb=0, stream=None)
     args.update(kw)
     return bros.LIB.bros_attn_decode(args["out"], args["q"], args["k"], args["v"], args["nb"], args["bt"],
-                                     args["maxb"], args["dir"], args["cls"], args["ctx"], args["max_ctx"],
+                                     args["maxb"], args["dir"], args["cls"], args["dpe"], args["ctx"], args["max_ctx"],
                                      args["S"], args["hq"], args["hkv"], args["d"], args["bs"], args["scale"],
                                      args["dtype"], args["ws"], args["wsb"], args["stream"])
 
@@ -68,6 +68,8 @@ def _decode(**kw):
     (dict(out=None), -1),
     (dict(bt=None), -1),
     (dict(dir=None, cls=None), -1),
+    (dict(dpe=2), -2),                 # direction mode neither per sequence nor per entry
+    (dict(dir=None, cls=FAKE, dpe=1), -1),   # a direction table needs dir
     (dict(S=-1), -2),
     (dict(nb=0), -2),
     (dict(maxb=0), -2),
@@ -85,26 +87,30 @@ def test_decode_with_no_sequences_is_a_noop():
 
 def test_kv_write_rejects():
     L = bros.LIB
-    args = [FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE, 4, FAKE, None, FAKE, FAKE, 2, 2, 128, 16, 1, None]
-    a = list(args); a[16] = 9
+    args = [FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE, 4, FAKE, None, 0, FAKE, FAKE, 2, 2, 128, 16, 1, None]
+    a = list(args); a[17] = 9
     assert L.bros_kv_write(*a) == -3
-    a = list(args); a[12] = 0
+    a = list(args); a[13] = 0
     assert L.bros_kv_write(*a) == -2
-    a = list(args); a[10] = None
+    a = list(args); a[11] = None
     assert L.bros_kv_write(*a) == -1
+    a = list(args); a[10] = 3
+    assert L.bros_kv_write(*a) == -2         # direction mode
     a = list(args); a[2] = 0
     assert L.bros_kv_write(*a) == 0          # no tokens: no-op
 
 
 def test_prefill_rejects():
     L = bros.LIB
-    base = [FAKE, FAKE, FAKE, 64, 32, FAKE, FAKE, 10, FAKE, 4, FAKE, None, FAKE, 64, 2, 8, 2, 128, 16,
+    base = [FAKE, FAKE, FAKE, 64, 32, FAKE, FAKE, 10, FAKE, 4, FAKE, None, 0, FAKE, 64, 2, 8, 2, 128, 16,
             0.0, 1, None, 0, None]
     a = list(base); a[4] = 0
     assert L.bros_attn_prefill_chunk(*a) == -2
     a = list(base); a[2] = None
     assert L.bros_attn_prefill_chunk(*a) == -1
-    a = list(base); a[20] = 0; a[13] = 100000   # fp32 path needs a workspace
+    a = list(base); a[10] = None; a[11] = FAKE; a[12] = 1   # a direction table needs dir
+    assert L.bros_attn_prefill_chunk(*a) == -1
+    a = list(base); a[21] = 0; a[14] = 100000   # fp32 path needs a workspace
     assert L.bros_attn_prefill_chunk(*a) == -5
     a = list(base); a[3] = 0
     assert L.bros_attn_prefill_chunk(*a) == 0
@@ -208,6 +214,37 @@ def test_checker_rejects(mutate, needle):
     with pytest.raises(bros.BrosError) as ei:
         bros.bros_check_batch(t, d, None, c, 4)
     assert ei.value.status == -7 and needle in str(ei.value)
+
+
+@pytest.mark.parametrize("config", [1, 2, 3, 5])
+def test_checker_accepts_direction_tables(config):
+    """The paper's per-entry direction table (Sec. 6): flipping entries of
+    blocks a sequence fills keeps the batch consistent, and the checker agrees
+    with the oracle's slot-ownership count."""
+    from tests.gpu_helpers import with_direction_table
+    b = with_direction_table(W.generate(config), frac=0.5, seed=config)
+    assert b.dir.ndim == 2
+    assert oracle.slot_owner_counts(b.block_tables, b.dir, b.ctx_lens, b.num_blocks).max() <= 1
+    bros.bros_check_batch(b.block_tables, b.dir, None, b.ctx_lens, b.num_blocks)
+
+
+def test_checker_rejects_bad_direction_tables():
+    # RT tail (5 slots from the left) and BE tail (11 from the right) share block 0
+    t = np.array([[2, 0], [3, 0]], dtype=np.int32)
+    c = np.array([21, 27], dtype=np.int32)
+    d = np.array([[1, 1], [-1, -1]], dtype=np.int8)
+    bros.bros_check_batch(t, d, None, c, 4)
+    bad = d.copy()
+    bad[0, 1] = -1                       # the RT tail walked from the right collides with the BE tail
+    with pytest.raises(bros.BrosError, match="already owned"):
+        bros.bros_check_batch(t, bad, None, c, 4)
+    assert oracle.slot_owner_counts(t, bad, c, 4).max() == 2
+    bad = d.copy()
+    bad[1, 0] = 0                        # not a direction
+    with pytest.raises(bros.BrosError, match="entry 0"):
+        bros.bros_check_batch(t, bad, None, c, 4)
+    with pytest.raises(ValueError):
+        bros.bros_check_batch(t, d[:, :1], None, c, 4)   # table shape must match
 
 
 def test_checker_rejects_unsupported_block_size():
