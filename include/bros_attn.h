@@ -83,7 +83,8 @@ enum bros_status {
   BROS_E_UNSUPPORTED = -4, /* block_size != 16, head_dim != 128, group not in {1,2,4,8} */
   BROS_E_WORKSPACE = -5,   /* workspace missing or smaller than the size query's answer */
   BROS_E_HIP = -6,         /* a HIP launch failed; message carries hipGetErrorString    */
-  BROS_E_TABLE = -7        /* bros_check_batch found an inconsistent batch               */
+  BROS_E_TABLE = -7,       /* bros_check_batch found an inconsistent batch               */
+  BROS_E_NOMEM = -8        /* the block manager found no block for a request            */
 };
 enum bros_workspace_kind { BROS_WS_DECODE = 0, BROS_WS_PREFILL = 1 };
 
@@ -314,6 +315,98 @@ int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_per_seq,
                      const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
                      int32_t num_seqs, int32_t num_blocks, int32_t block_size,
                      int32_t check_slot_disjointness);
+
+/*
+ * HOST BLOCK MANAGER AND SCHEDULER (host memory only; no GPU calls)
+ *
+ * Defines: Sec. 5.2 (Block Management): FindBlock places a request's KV in the
+ * blocks with the most empty slots (a free block first); for RT requests
+ * FindPreemptBlock takes BE blocks, again those with the most empty slots,
+ * and writes from the opposite end; once a shared block's slots run out, only
+ * the peer tokens about to be overwritten are checkpointed (lazy
+ * checkpointing), the block enters the preemption table, and the tokens come
+ * back when their request is scheduled again. Sec. 4.2: Alg. 1 (priority-
+ * based packing) and adaptive batch sizing.
+ *
+ * Readings where the paper is silent: a request's entry e always holds its
+ * positions [16 e, 16 e + 16) (the exclusive view); an RT token that meets a
+ * BE token checkpoints it, while a BE token that meets an RT token moves the
+ * BE entry to another block (BE never overwrites RT); a restored entry stays
+ * in place when its missing slots are free, else it moves with its tokens.
+ *
+ * Ownership: a manager handle is created and destroyed by the caller; it is
+ * not thread-safe. Plans name slots by id (block * 16 + slot).
+ */
+typedef struct bros_mgr_plan {
+  int32_t* victims;      /* [victims_cap][4]: request, position, block, slot -- checkpoint BEFORE the write */
+  int32_t victims_cap, num_victims;
+  int32_t* move_src;     /* [moves_cap] slot ids: device moves (gather src -> scatter dst) BEFORE the write */
+  int32_t* move_dst;
+  int32_t moves_cap, num_moves;
+  int32_t* restore_pos;  /* [restores_cap] positions of the request whose checkpointed rows come back */
+  int32_t* restore_dst;  /* ... to these slot ids (after the moves) */
+  int32_t restores_cap, num_restores;
+  int32_t* written_pos;  /* [written_cap] position and slot id of every new token (grow only) */
+  int32_t* written_slot;
+  int32_t written_cap, num_written;
+} bros_mgr_plan;
+
+void* bros_mgr_create(int32_t num_blocks);                 /* NULL on error (bros_last_error) */
+void bros_mgr_destroy(void* mgr);
+int bros_mgr_add_request(void* mgr, int32_t req, int32_t cls);
+int bros_mgr_release(void* mgr, int32_t req);             /* frees its slots; drops its checkpoints */
+/* n_new more tokens for req (FindBlock / FindPreemptBlock, lazy checkpoints,
+ * BE relocations). Fails with BROS_E_TABLE if req still has checkpointed
+ * tokens (restore first) and BROS_E_NOMEM when blocks run out (tokens placed
+ * before that stay placed and are reported in the plan). BROS_E_SHAPE if a
+ * plan buffer is too small (the plan's counts give the sizes needed). */
+int bros_mgr_grow(void* mgr, int32_t req, int32_t n_new, bros_mgr_plan* plan);
+/* Brings req's checkpointed tokens back: moves and restore destinations. */
+int bros_mgr_restore(void* mgr, int32_t req, bros_mgr_plan* plan);
+int bros_mgr_query(void* mgr, int32_t req, int32_t* ctx, int32_t* num_entries, int32_t* checkpointed);
+int bros_mgr_table(void* mgr, int32_t req, int32_t* out, int32_t cap);
+int32_t bros_mgr_free_blocks(void* mgr);
+/* Checks every internal invariant of the manager (owners and entries agree,
+ * counts fit, block lists match block states); BROS_E_TABLE names the first
+ * broken one. For tests and debugging; it walks every block. */
+int bros_mgr_validate(void* mgr);
+int32_t bros_mgr_available(void* mgr, int32_t cls);       /* blocks a new entry of class cls may take */
+int32_t bros_mgr_entries_needed(void* mgr, int32_t req, int32_t n_new);
+/* Preemption table: [n][3] (block, RT owner, BE owner) of blocks in preemption
+ * status, up to cap rows; returns the total count. */
+int32_t bros_mgr_preemption_table(void* mgr, int32_t* out, int32_t cap);
+
+/* A queued request as Alg. 1 sees it. */
+typedef struct bros_sched_req {
+  int32_t id;
+  int32_t prefill;       /* 1: prefill phase, 0: decode phase */
+  int32_t n_new;         /* input tokens this iteration (Ln contribution) */
+  int32_t ctx_after;     /* attended tokens after this iteration (La contribution) */
+  double remaining_us;   /* RT: T_SLO - t_i - (k_i - 1) T_avg (sort key); BE: unused */
+  int32_t m_cpu;         /* BE: checkpointed slots (sort key); RT: unused */
+} bros_sched_req;
+
+/* C(batch) of Sec. 4.1 per phase: coef[0] prefill, coef[1] decode, each
+ * {a0, a1, b} in microseconds; per_request = 0 uses Ln * La, 1 uses the sum
+ * of n_i * a_i as the interaction term. */
+typedef struct bros_cost_model {
+  double coef[2][3];
+  int32_t per_request;
+} bros_cost_model;
+
+/* Alg. 1 for one iteration: RT requests by ascending remaining time while the
+ * batch has room, blocks exist (FindPreemptBlock) and the estimated time stays
+ * within the most urgent request's remaining time; then BE requests by
+ * ascending m_cpu, packed while they fit, else replacing the least urgent
+ * RT request. Writes the chosen ids (rt_ready / be_ready must hold n_rt /
+ * n_be ids) and over_budget = 1 when the time budget stopped the RT loop. The
+ * manager is only read. */
+int bros_schedule(void* mgr, const bros_sched_req* rt, int32_t n_rt, const bros_sched_req* be, int32_t n_be,
+                  int32_t batch_size, const bros_cost_model* cost, int32_t* rt_ready, int32_t* n_rt_ready,
+                  int32_t* be_ready, int32_t* n_be_ready, int32_t* over_budget);
+/* Adaptive batch sizing: back to `base` after an over-budget iteration, else
+ * doubled (at most max_size). */
+int32_t bros_next_batch_size(int32_t current, int32_t base, int32_t max_size, int32_t over_budget);
 
 #ifdef __cplusplus
 }

@@ -20,12 +20,16 @@ BROS_F32, BROS_BF16 = 0, 1
 BROS_RT, BROS_BE = 0, 1
 BROS_WS_DECODE, BROS_WS_PREFILL = 0, 1
 STATUS = {0: "BROS_OK", -1: "BROS_E_NULL", -2: "BROS_E_SHAPE", -3: "BROS_E_DTYPE",
-          -4: "BROS_E_UNSUPPORTED", -5: "BROS_E_WORKSPACE", -6: "BROS_E_HIP", -7: "BROS_E_TABLE"}
+          -4: "BROS_E_UNSUPPORTED", -5: "BROS_E_WORKSPACE", -6: "BROS_E_HIP", -7: "BROS_E_TABLE",
+          -8: "BROS_E_NOMEM"}
 
 EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_write",
             "bros_attn_decode", "bros_attn_prefill_chunk", "bros_attn_workspace_size",
             "bros_check_batch", "bros_stream_create_cu_share", "bros_stream_destroy",
-            "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma"]
+            "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma",
+            "bros_mgr_create", "bros_mgr_destroy", "bros_mgr_add_request", "bros_mgr_release", "bros_mgr_grow",
+            "bros_mgr_restore", "bros_mgr_query", "bros_mgr_table", "bros_mgr_free_blocks", "bros_mgr_validate", "bros_mgr_available",
+            "bros_mgr_entries_needed", "bros_mgr_preemption_table", "bros_schedule", "bros_next_batch_size"]
 
 
 class BrosError(RuntimeError):
@@ -71,6 +75,8 @@ def _load() -> ctypes.CDLL:
     lib.bros_check_slot_ids.restype = ctypes.c_int
     lib.bros_copy_dma.argtypes = [P, P, Z, P]
     lib.bros_copy_dma.restype = ctypes.c_int
+    from . import manager as _m   # host block manager and scheduler signatures
+    _m.declare(lib)
     return lib
 
 

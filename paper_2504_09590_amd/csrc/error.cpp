@@ -41,12 +41,13 @@ const char* bros_status_str(int status) {
     case BROS_E_WORKSPACE: return "BROS_E_WORKSPACE";
     case BROS_E_HIP: return "BROS_E_HIP";
     case BROS_E_TABLE: return "BROS_E_TABLE";
+    case BROS_E_NOMEM: return "BROS_E_NOMEM";
     default: return "BROS_E_UNKNOWN";
   }
 }
 
 const char* bros_last_error(void) { return g_last_error.c_str(); }
 
-int bros_abi_version(void) { return 5; }
+int bros_abi_version(void) { return 6; }
 
 }  // extern "C"

@@ -31,6 +31,7 @@ Ordering, all on the device (no host synchronisation):
 
 from __future__ import annotations
 
+import numpy as np
 import torch
 
 from . import bros
@@ -129,3 +130,65 @@ class SwapLane:
             return
         self._copy_done.record(self.copy)
         stream.wait_event(self._copy_done)
+
+
+class PlanExecutor:
+    """Carries out a block manager's plan (paper_2504_09590_amd.manager) on the
+    device, on one stream, in the order the plan requires: the victims are
+    gathered and copied to pinned host memory, relocated entries are moved
+    (gather into staging, scatter to their new slots), and checkpointed rows
+    come back (host to staging, scatter). The step's kv_write follows. Rows
+    are kept on the host per (request, position) until restored."""
+
+    def __init__(self, k_pool, v_pool, max_rows: int):
+        import torch
+        hkv, d = k_pool.shape[1], k_pool.shape[3]
+        self.k_pool, self.v_pool = k_pool, v_pool
+        self.max_rows = int(max_rows)
+        shape = (self.max_rows, hkv, d)
+        self.sk = torch.empty(shape, dtype=k_pool.dtype, device=k_pool.device)
+        self.sv = torch.empty(shape, dtype=k_pool.dtype, device=k_pool.device)
+        self.hk = torch.empty(shape, dtype=k_pool.dtype, pin_memory=True)
+        self.hv = torch.empty(shape, dtype=k_pool.dtype, pin_memory=True)
+        self.store = {}        # (request, position) -> (K row, V row) on the host
+        self._row = self.sk[0].numel() * self.sk.element_size()
+
+    def _ids(self, ids):
+        import torch
+        return torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).to(self.k_pool.device)
+
+    def execute(self, req: int, plan, stream=None) -> None:
+        import torch
+        stream = stream if stream is not None else torch.cuda.current_stream()
+        for lo in range(0, len(plan.victims), self.max_rows):
+            part = plan.victims[lo:lo + self.max_rows]
+            n = len(part)
+            ids = self._ids(part[:, 2] * 16 + part[:, 3])
+            bros.bros_kv_gather(self.k_pool, self.v_pool, ids, self.sk, self.sv, num_slots=n, stream=stream)
+            bros.bros_copy_dma(self.hk, self.sk, n * self._row, stream=stream)
+            bros.bros_copy_dma(self.hv, self.sv, n * self._row, stream=stream)
+            stream.synchronize()
+            for i, (r, p, _, _) in enumerate(part):
+                self.store[(int(r), int(p))] = (self.hk[i].clone(), self.hv[i].clone())
+        for lo in range(0, len(plan.move_src), self.max_rows):
+            src, dst = plan.move_src[lo:lo + self.max_rows], plan.move_dst[lo:lo + self.max_rows]
+            bros.bros_kv_gather(self.k_pool, self.v_pool, self._ids(src), self.sk, self.sv, num_slots=len(src),
+                                stream=stream)
+            bros.bros_kv_scatter(self.sk, self.sv, self._ids(dst), self.k_pool, self.v_pool, num_slots=len(dst),
+                                 stream=stream)
+        for lo in range(0, len(plan.restore_pos), self.max_rows):
+            pos, dst = plan.restore_pos[lo:lo + self.max_rows], plan.restore_dst[lo:lo + self.max_rows]
+            stream.synchronize()                      # the host rows are reused below
+            for i, p in enumerate(pos):
+                k, v = self.store.pop((int(req), int(p)))
+                self.hk[i].copy_(k)
+                self.hv[i].copy_(v)
+            n = len(pos)
+            bros.bros_copy_dma(self.sk, self.hk, n * self._row, stream=stream)
+            bros.bros_copy_dma(self.sv, self.hv, n * self._row, stream=stream)
+            bros.bros_kv_scatter(self.sk, self.sv, self._ids(dst), self.k_pool, self.v_pool, num_slots=n,
+                                 stream=stream)
+
+    def drop(self, req: int) -> None:
+        for key in [k for k in self.store if k[0] == req]:
+            del self.store[key]

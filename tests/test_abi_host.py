@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings_and_version():
     for code, name in bros.STATUS.items():
         assert bros.LIB.bros_status_str(code).decode() == name
-    assert bros.LIB.bros_abi_version() == 5
+    assert bros.LIB.bros_abi_version() == 6
 
 
 # --- argument validation (returns before any HIP call) -----------------------
