@@ -5,14 +5,18 @@
 // sequence s sits at position c0 + j, c0 = ctx - n, and attends to positions
 // 0 .. c0 + j of the sequence, gathered from the bidirectional pool (Sec. 5.1).
 //
-// Work units. A workgroup (8 waves, two per SIMD) owns one (sequence, KV
+// Work units. A workgroup (4 waves, one per SIMD) owns one (sequence, KV
 // head, tile of 128 / G positions): 128 query rows, all G = Hq / Hkv query
 // heads of that KV head. Waves 0-3 take rows 0-31, 32-63, 64-95, 96-127 over
-// the even 32-key tiles of the context, waves 4-7 the same rows over the odd
-// tiles, so a unit's chain is half its key tiles long; the two halves are
-// merged through LDS at the end. Two waves per SIMD let one wave's vector
-// work (the softmax) run beside the other's matrix-core products: a single
-// wave issues vector instructions at about half the rate two waves reach.
+// all the key tiles of the context. Two workgroups share a compute unit (77
+// KiB of LDS each, two waves per SIMD), and they run unsynchronised: one
+// wave's vector work (the softmax) runs beside the other's matrix-core
+// products -- a single wave issues vector instructions at about half the rate
+// two waves reach -- and one unit's start-up (lengths, Q, first tiles) hides
+// behind the other's steps. (With kHalves = 2 the kernel instead runs 8 waves
+// per workgroup that split the key tiles in two halves merged through LDS at
+// the end, one workgroup per unit and per compute unit; on MI355X that is
+// about 10 % slower.)
 // Workgroups are launched longest unit first (ranked on the device from the
 // length table), and consecutive ids are spread over the XCDs so that one KV
 // head of every sequence stays on one XCD's L2.
@@ -23,7 +27,8 @@
 // and the transposing V^T reads (ds_read_b64_tr_b16) free of bank conflicts.
 // K and V have rings of their own (four slots each): the K tile of step i + 1
 // is read while the V tile of step i is, and each slot is refilled four steps
-// ahead of its use. Table entries arrive as scalar loads a step ahead.
+// ahead of its use. The unit's table entries are validated once into LDS and
+// read a step ahead of the loads that use them.
 //
 // Software pipeline (per wave, per step): the scores S^T = K Q^T of the next
 // tile are computed on the matrix cores while the vector ALU turns the current
@@ -58,7 +63,11 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 512;                       // 8 waves: two per SIMD
+// Key halves per workgroup: 2 = 8 waves (two per SIMD) splitting a unit's key
+// tiles between two wave sets; 1 = 4 waves (one per SIMD) each taking all of
+// its rows' key tiles, two workgroups sharing a compute unit.
+constexpr int kHalves = 1;
+constexpr int kThreads = 256 * kHalves;
 constexpr int kRows = 128;                         // query rows per workgroup
 constexpr int kKeys = 32;                          // keys per tile (2 blocks)
 constexpr int kSlots = 4;                          // stages of the K ring and of the V ring
@@ -144,13 +153,13 @@ __device__ __forceinline__ int unit_tiles(const PrefillArgs& a, int s, int t, in
 }
 
 template <int G>
-__global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(PrefillArgs a) {
   constexpr int QT = kRows / G;   // positions per unit
   // K ring and V ring, kSlots slots each; a slot holds the even-tile half and
   // the odd-tile half (kTileBytes each). Slot offsets are compile-time
   // constants below 64 KiB, so they fold into the LDS instructions' offset
   // field.
-  constexpr int kSlotBytes = 2 * kTileBytes;
+  constexpr int kSlotBytes = kHalves * kTileBytes;
   __shared__ __attribute__((aligned(1024))) uint8_t s_kring[kSlots * kSlotBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t s_vring[kSlots * kSlotBytes];
   __shared__ int s_first_bad;
@@ -163,7 +172,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   const int lane = tid & (kWave - 1);
   const int wv = wave_id_uniform();
   const int rg = wv & 3;    // row group: rows 32 rg .. 32 rg + 31
-  const int kh = wv >> 2;   // key half: tiles kh, kh + 2, kh + 4, ...
+  const int kh = kHalves == 2 ? (wv >> 2) : 0;   // key half: tiles kh, kh + kHalves, ...
 
   // ---- Which unit: rank by key tiles, longest first (ties by index). Ids
   // r * Hkv + g give every rank all KV heads on consecutive ids, i.e. on
@@ -226,8 +235,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
   // keys below this logical position are visible to every row of the unit
   const int full_below = min(ctx, c0 + t0 + 1);
-  const int n_steps = (n_kt + 1) / 2;        // both halves step together
-  const int n_mine = (n_kt - kh + 1) / 2;     // tiles of this wave's half
+  const int n_steps = (n_kt + kHalves - 1) / kHalves;        // both halves step together
+  const int n_mine = (n_kt - kh + kHalves - 1) / kHalves;     // tiles of this wave's half
 
   const int half = lane >> 5;
   const int mrow = lane & 31;
@@ -269,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   // Read a step ahead of its use; the value comes back in a vector register
   // and is made scalar where it is used.
   auto own = [&](int j) -> int {
-    const int b = 2 * (2 * j + kh) + my_bt;
+    const int b = 2 * (kHalves * j + kh) + my_bt;
     return b < nblk ? s_tbl[b] : -1;
   };
   auto valid = [&](int j, int v) -> int { return __builtin_amdgcn_readfirstlane(v); };
@@ -288,7 +297,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   }
   auto issue = [&](int j, int raw, const uint16_t* pool, uint8_t* ring) __attribute__((always_inline)) {
     const int blk = valid(j, raw);
-    const int b = (2 * j + kh < n_kt && blk >= 0) ? blk : 0;
+    const int b = (kHalves * j + kh < n_kt && blk >= 0) ? blk : 0;
     const uint16_t* base = pool + ((size_t)b * Hkv + g) * kBlockSize * kHeadDim;
     uint8_t* dst = ring + kh * kTileBytes + 8 * rg * kRowBytes;
 #pragma unroll
@@ -297,7 +306,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   // Once this wave's V loads of step j have landed: zero its rows whose slot
   // is not context.
   auto fixup_v = [&](int j, int raw, uint8_t* ring) __attribute__((always_inline)) {
-    const int tile = 2 * j + kh;
+    const int tile = kHalves * j + kh;
     if (tile >= n_kt) return;
     const int blk = valid(j, raw);
     const int b = 2 * tile + my_bt;
@@ -333,12 +342,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   for (int dt = 0; dt < 4; ++dt) o[dt] = floatx16{};
   float m_run = kNoMax, l_run = 0.0f, alpha = 1.0f;
   // Raw scores of the wave's next tile, carried from the step that computes
-  // them (and their max) to the step that turns them into probabilities.
+  // them (and their max) to the step that turns them into probabilities: two
+  // buffers, so that a step reads one while the matrix cores write the other
+  // (the unrolled main loop alternates them; elsewhere `sa` is the carried one).
   // Every accumulator here lives in vector registers: with no accumulation
   // register in use, the compiler gives the wave its whole register budget as
   // vector registers and the matrix cores write their results there, so the
   // vector ALU reads scores and rescales O directly.
-  floatx16 cur;
+  floatx16 sa, sb;
   const float sl2 = a.scale_log2;
 
   // K operands of the tile in K ring `sk` (this wave's half), all eight
@@ -353,14 +364,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     for (int c = 0; c < 8; ++c)
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[c]), qf[c], c == 0 ? floatx16{} : acc, 0, 0, 0);
   };
-  // Take the accumulators as `cur`, mask them (when asked: `tile` is the
-  // tile they belong to) and fold the tile's max into the running max; sets
-  // alpha, the factor O and l take for the new max. Accumulator j is key
+  // Mask the accumulators in place (when asked: `tile` is the tile they
+  // belong to) and fold the tile's max into the running max; sets alpha, the
+  // factor O and l take for the new max. Accumulator j is key
   // k = 8*(j/4) + 4*half + j%4 of the tile: physical slot k % 16 of the
   // tile's block k / 16, which holds that block's position offset
   // slot_of_offset(k % 16, dir).
-  auto mask_max = [&](floatx16& acc, auto maskc, int tile) __attribute__((always_inline)) {
-    cur = acc;
+  auto mask_max = [&](floatx16& cur, auto maskc, int tile) __attribute__((always_inline)) {
     if constexpr (decltype(maskc)::value) {
       // visible: valid block, position < ctx and <= the row's position
       const int lim = min(qpos, ctx - 1);
@@ -390,7 +400,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   // weights the PV product applies. Operand c2 (16 keys) holds accumulators
   // 8*c2 .. 8*c2 + 7.
   const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
-  auto probs = [&](bf16x8_t (&pf)[2]) __attribute__((always_inline)) {
+  auto probs = [&](bf16x8_t (&pf)[2], const floatx16& cur) __attribute__((always_inline)) {
     float psum = l_run;
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2) {
@@ -441,8 +451,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   // while the vector ALU forms the current probabilities; then the PV
   // products run while the new scores are moved, masked and maxed. The other
   // wave on the SIMD fills the gaps.
-  auto step = [&](const uint8_t* sk, const uint8_t* sv, int next_tile, auto has_next, auto mask_next)
-                  __attribute__((always_inline)) {
+  // `in` holds the current tile's scores, `out` receives the next tile's.
+  auto step = [&](const uint8_t* sk, const uint8_t* sv, int next_tile, auto has_next, auto mask_next,
+                  const floatx16& in, floatx16& out) __attribute__((always_inline)) {
     constexpr bool NEXT = decltype(has_next)::value;
     v4u_t kv[8];
     v4u_t vv0[4], vv1[4];
@@ -450,14 +461,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     v_operands(sv, 0, vv0);
     __builtin_amdgcn_sched_barrier(0);
     bf16x8_t pf[2];
-    floatx16 acc;
-    if constexpr (NEXT) scores(kv, acc);
-    probs(pf);
+    if constexpr (NEXT) scores(kv, out);
+    probs(pf, in);
     v_operands(sv, 1, vv1);
     __builtin_amdgcn_sched_barrier(0);
     pv(vv0, pf, 0);
     pv(vv1, pf, 1);
-    if constexpr (NEXT) mask_max(acc, mask_next, next_tile);
+    if constexpr (NEXT) mask_max(out, mask_next, next_tile);
   };
   // After step ii: wait for batch ii + 1 (K of step ii + 2, V of step ii + 1),
   // zero V's non-context rows (FIX; a tile below plain_tiles has none),
@@ -482,7 +492,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   // the first scores are in. Table entries run ahead of their use in a
   // window: w0 .. w4 hold this wave's entries for steps ii + 1 .. ii + 5.
   // (the first entries as scalar loads: the LDS copy is made while they load)
-  auto own0 = [&](int j) -> int { return entry(2 * (2 * j + kh) + my_bt); };
+  auto own0 = [&](int j) -> int { return entry(2 * (kHalves * j + kh) + my_bt); };
   const int e0 = own0(0);
   int w0 = own0(1), w1 = own0(2), w2 = own0(3), w3 = own0(4), w4 = own0(5);
   issue(0, e0, kpool, s_kring);
@@ -511,11 +521,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   lds_barrier();
   if (n_mine > 0) {
     v4u_t kv[8];
-    floatx16 acc;
     k_operands(kr, kv);
-    scores(kv, acc);
-    if (kh >= plain_tiles) mask_max(acc, std::true_type{}, kh);
-    else mask_max(acc, std::false_type{}, kh);
+    scores(kv, sa);
+    if (kh >= plain_tiles) mask_max(sa, std::true_type{}, kh);
+    else mask_max(sa, std::false_type{}, kh);
   }
   lds_barrier();   // K slot 0 is free again
   issue(2, w1, kpool, s_kring + 2 * kSlotBytes);
@@ -542,12 +551,16 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     w4 = nw;
   };
   // this wave's tiles 2 j + kh below plain_tiles, as a step bound
-  const int n_plain = min(n_mine, (plain_tiles - kh + 1) / 2);
+  const int n_plain = min(n_mine, (plain_tiles - kh + kHalves - 1) / kHalves);
   auto main_step = [&](auto uc) __attribute__((always_inline)) -> bool {
     constexpr int u = decltype(uc)::value;
     if (ii + 1 >= n_plain) return false;
     const int nw = own(ii + 6);
-    step(kr + ((u + 1) % kSlots) * kSlotBytes, vr + u * kSlotBytes, 0, std::true_type{}, std::false_type{});
+    // step ii reads buffer ii % 2 and fills the other (u and ii agree mod 4)
+    if constexpr (u % 2 == 0)
+      step(kr + ((u + 1) % kSlots) * kSlotBytes, vr + u * kSlotBytes, 0, std::true_type{}, std::false_type{}, sa, sb);
+    else
+      step(kr + ((u + 1) % kSlots) * kSlotBytes, vr + u * kSlotBytes, 0, std::true_type{}, std::false_type{}, sb, sa);
     rescale_o();
     advance(ii, u, w0, w3, w4, std::false_type{});
     shift(nw);
@@ -556,12 +569,15 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   };
   while (main_step(Int<0>{}) && main_step(Int<1>{}) && main_step(Int<2>{}) && main_step(Int<3>{})) {
   }
+  if (ii & 1) sa = sb;   // the rest carries the scores in `sa`
   // Tiles with a next tile that needs (or may need) the mask.
   for (; ii + 1 < n_mine; ++ii) {
     const int sl = ii & (kSlots - 1);
     const int sl1 = (sl + 1) & (kSlots - 1);
     const int nw = own(ii + 6);
-    step(kr + sl1 * kSlotBytes, vr + sl * kSlotBytes, 2 * (ii + 1) + kh, std::true_type{}, std::true_type{});
+    step(kr + sl1 * kSlotBytes, vr + sl * kSlotBytes, kHalves * (ii + 1) + kh, std::true_type{}, std::true_type{}, sa,
+         sb);
+    sa = sb;
     rescale_o();
     advance(ii, sl, w0, w3, w4, std::true_type{});
     shift(nw);
@@ -570,7 +586,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
   if (ii < n_mine) {
     const int sl = ii & (kSlots - 1);
     const int nw = own(ii + 6);
-    step(kr, vr + sl * kSlotBytes, 0, std::false_type{}, std::false_type{});
+    step(kr, vr + sl * kSlotBytes, 0, std::false_type{}, std::false_type{}, sa, sb);
     advance(ii, sl, w0, w3, w4, std::true_type{});
     shift(nw);
     ++ii;
@@ -582,9 +598,29 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
     shift(nw);
   }
 
+  wait_vmem<0>();
+  if constexpr (kHalves == 1) {
+    // ---- One key set: normalise and write the rows.
+    l_run = pair_sum(l_run);
+    const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+    if (row_valid) {
+      uint16_t* op = static_cast<uint16_t*>(a.out) + row_off;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+        for (int jq = 0; jq < 4; ++jq) {
+          const int d0 = 32 * dt + 8 * jq + 4 * half;   // accumulators 4jq..4jq+3 are dims d0..d0+3
+          uint2 w;
+          w.x = pack2_bf16(o[dt][4 * jq + 0] * inv, o[dt][4 * jq + 1] * inv);
+          w.y = pack2_bf16(o[dt][4 * jq + 2] * inv, o[dt][4 * jq + 3] * inv);
+          *reinterpret_cast<uint2*>(op + d0) = w;
+        }
+      }
+    }
+    return;
+  } else {
   // ---- Merge the two key halves through LDS (K ring reused once every load
   // has landed and every wave is past the last step) and write the rows.
-  wait_vmem<0>();
   lds_barrier();
   l_run = pair_sum(l_run);
   float* xo = reinterpret_cast<float*>(s_kring + rg * kSlotBytes);   // per row group: [dt][jq][lane] float4 = 16 KB
@@ -624,6 +660,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_mfma_kernel(PrefillArgs a
         }
       }
     }
+  }
   }
 }
 
