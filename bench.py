@@ -45,10 +45,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("77b380571deae4407a3cbc626c03b38e257709410c08d5349fedad2186e4057b", 5096180.2, 25492.2),
-    "llama3-8b-decode": ("77b380571deae4407a3cbc626c03b38e257709410c08d5349fedad2186e4057b", 463949.2, 9333.0),
-    "llama3-8b-mixed-step": ("77b380571deae4407a3cbc626c03b38e257709410c08d5349fedad2186e4057b", 1152761.9, 10362.0),
-    "llama3-8b-pressure": ("77b380571deae4407a3cbc626c03b38e257709410c08d5349fedad2186e4057b", 622326.9, 15234.4),
+    "llama3-70b-decode": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 5093760.9, 25491.8),
+    "llama3-8b-decode": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 463938.6, 9332.6),
+    "llama3-8b-mixed-step": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 1152544.9, 10362.9),
+    "llama3-8b-pressure": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 622034.6, 15235.7),
 }
 
 
