@@ -11,15 +11,20 @@
 // max-rescaling.
 //
 // Work. A tile is one (row, KV head, 16-slot block); a (row, KV head) pair is
-// a segment of consecutive tiles. The grid holds what the chip keeps resident
-// at four waves per SIMD, and every wave is an independent worker that takes
-// an equal contiguous share of all tiles in (row, KV head, block) order, so
-// the load is balanced to within one tile whatever the mix of context
-// lengths. A worker walks its share tile by tile: the next tile's K and V are
-// requested as soon as this tile's registers are free (the next tile may
-// start a new segment), and block-table entries come through the scalar
-// cache one tile ahead so they never wait behind KV loads. KV tiles are read
-// with non-temporal loads; each byte of the KV pool is read once.
+// a segment of consecutive tiles. The grid holds what the compute units of
+// the stream keep resident at two waves per SIMD, and every wave is an
+// independent worker that takes an equal contiguous share of all tiles in
+// (row, KV head, block) order, so the load is balanced to within one tile
+// whatever the mix of context lengths. A worker walks its share tile by tile
+// with kDepth register sets for K and V: while it computes tile i, the loads
+// of the next kDepth - 1 tiles are in flight, and tile i + kDepth's are
+// requested into tile i's set as soon as those registers are read (a tile may
+// start a new segment). Fewer waves with more tiles in flight each move more
+// bytes than more waves with one tile each: two waves per SIMD with two tiles
+// in flight beat four waves with one by 5-8 %, and a third tile adds nothing.
+// Block-table entries come through the scalar cache one tile before their
+// loads issue. KV tiles are read with non-temporal loads; each byte of the KV
+// pool is read once.
 //
 // A segment that lies wholly inside one worker's share is normalised and
 // written by that worker. A segment cut between workers leaves one partial
@@ -35,11 +40,14 @@
 #include "decode_common.h"
 
 #include <mutex>
+#include <type_traits>
 
 namespace bros {
 namespace {
 
 constexpr int kMaxSplitBlocks = 64;   // fp32 split-K: blocks per split at most
+// Tiles whose K/V loads a bf16 decode wave keeps in flight (register sets).
+constexpr int kDepth = 2;
 
 // ---------------------------------------------------------------------------
 // bf16 decode on the matrix cores. Per 16-slot block of one (row, KV head), the
@@ -167,7 +175,7 @@ __device__ __forceinline__ int worker_of(int64_t tile, int64_t total, int64_t wo
 }
 
 template <int G>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void decode_mfma_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_mfma_kernel(DecodeArgs a) {
   static_assert(G >= 1 && G <= 16, "heads of a group must fit the 16 MFMA columns");
   __shared__ int s_pre[kMaxRowsLds + 1];
   __shared__ int s_scan[kThreads];
@@ -195,7 +203,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 
   const uint32_t k_lane = (uint32_t)col * kHeadDim + 8 * grp;        // + 32 c
   const uint32_t v_lane = (uint32_t)(4 * grp) * kHeadDim + 8 * col;  // + j * kHeadDim
-  v4u_t qf[4], kf[4], vf[4];
+  // kDepth K/V register sets: tile i uses set i % kDepth while the loads of
+  // tiles i + 1 .. i + kDepth - 1 are in flight in the others, and tile
+  // i + kDepth's are issued into set i % kDepth as soon as its registers are
+  // read.
+  v4u_t qf[4], kf_[kDepth][4], vf_[kDepth][4];
   floatx4_t acc[8];
   float m_ref = kNoMax, l_part = 0.0f;
 
@@ -203,13 +215,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const int blk = load_uniform(a.block_tables, (size_t)c.s * a.max_blocks_per_seq + c.b);
     return (blk >= 0 && blk < a.num_blocks) ? blk : -1;
   };
-  auto issue_k = [&](int blk, int g) {
+  auto issue_k = [&](v4u_t (&kf)[4], int blk, int g) {
     if (blk < 0) return;
     const size_t base = ((size_t)blk * nkv + g) * kTileElems + k_lane;
 #pragma unroll
     for (int c = 0; c < 4; ++c) kf[c] = load_nt(a.k_pool, base + 32 * c);
   };
-  auto issue_v = [&](int blk, int g) {
+  auto issue_v = [&](v4u_t (&vf)[4], int blk, int g) {
     if (blk < 0) return;
     const size_t base = ((size_t)blk * nkv + g) * kTileElems + v_lane;
 #pragma unroll
@@ -224,29 +236,43 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
   };
 
-  Cursor c0, c1;
-  locate(a, s_pre, chunk, nch, t0, c0);
-  int blk0 = table(c0);
-  issue_k(blk0, c0.g);
-  issue_v(blk0, c0.g);
-  load_q(c0);
-  bool whole = c0.b == 0;   // this wave saw the segment's first tile
-  c1 = c0;
-  int blk1 = -1;
-  if (n > 1) {
-    advance(a, c1);
-    blk1 = table(c1);
+  // cur[d] / blk[d]: tile i + d (entries read one tile before their loads issue)
+  Cursor cur[kDepth + 2];
+  int blk[kDepth + 2];
+  locate(a, s_pre, chunk, nch, t0, cur[0]);
+  blk[0] = table(cur[0]);
+  issue_k(kf_[0], blk[0], cur[0].g);
+  issue_v(vf_[0], blk[0], cur[0].g);
+  load_q(cur[0]);
+  bool whole = cur[0].b == 0;   // this wave saw the segment's first tile
+#pragma unroll
+  for (int d = 1; d <= kDepth; ++d) {
+    cur[d] = cur[d - 1];
+    blk[d] = -1;
+    if (d < n) {
+      advance(a, cur[d]);
+      blk[d] = table(cur[d]);
+      if (d < kDepth) {
+        issue_k(kf_[d], blk[d], cur[d].g);
+        issue_v(vf_[d], blk[d], cur[d].g);
+      }
+    }
   }
+  blk[kDepth + 1] = -1;
+  cur[kDepth + 1] = cur[kDepth];
 #pragma unroll
   for (int t = 0; t < 8; ++t) acc[t] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-  for (int i = 0; i < n; ++i) {
-    // the tile after next: its table entry is read now, used one tile later
-    Cursor c2 = c1;
-    int blk2 = -1;
-    if (i + 2 < n) {
-      advance(a, c2);
-      blk2 = table(c2);
+  // Tile i, its K/V in (kf, vf).
+  auto body = [&](int i, v4u_t (&kf)[4], v4u_t (&vf)[4]) __attribute__((always_inline)) {
+    Cursor& c0 = cur[0];
+    const int blk0 = blk[0];
+    // the tile kDepth + 1 ahead: its table entry is read now, used one tile later
+    cur[kDepth + 1] = cur[kDepth];
+    blk[kDepth + 1] = -1;
+    if (i + kDepth + 1 < n) {
+      advance(a, cur[kDepth + 1]);
+      blk[kDepth + 1] = table(cur[kDepth + 1]);
     }
     floatx4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
     if (blk0 >= 0) {
@@ -256,11 +282,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                                                      __builtin_bit_cast(bf16x8_t, qf[k]), sc, 0, 0, 0);
     }
     const bool seg_end = c0.b == c0.nblk - 1 || i + 1 == n;
-    // K and query registers are free: the next tile's keys (and query on a new segment)
-    if (i + 1 < n) {
-      issue_k(blk1, c1.g);
-      if (seg_end) load_q(c1);
-    }
+    // K and query registers are free: keys kDepth tiles ahead (and the query
+    // of the next tile's segment)
+    if (i + kDepth < n) issue_k(kf, blk[kDepth], cur[kDepth].g);
+    if (i + 1 < n && seg_end) load_q(cur[1]);
     if (blk0 >= 0) {
       float s[4];
 #pragma unroll
@@ -303,8 +328,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, uint2{lo, hi}), pb, acc[t], 0, 0, 0);
       }
     }
-    // V registers are free: the next tile's values
-    if (i + 1 < n) issue_v(blk1, c1.g);
+    // V registers are free: values kDepth tiles ahead
+    if (i + kDepth < n) issue_v(vf, blk[kDepth], cur[kDepth].g);
 
     if (seg_end) {
       // The four lane groups of a head hold disjoint slots: total their weights.
@@ -343,10 +368,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
       for (int t = 0; t < 8; ++t) acc[t] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
       whole = true;
     }
-    c0 = c1;
-    blk0 = blk1;
-    c1 = c2;
-    blk1 = blk2;
+#pragma unroll
+    for (int d = 0; d <= kDepth; ++d) {
+      cur[d] = cur[d + 1];
+      blk[d] = blk[d + 1];
+    }
+  };
+  auto group = [&](int i, auto dc) __attribute__((always_inline)) -> bool {
+    constexpr int d = decltype(dc)::value;
+    if (i + d >= n) return false;
+    body(i + d, kf_[d], vf_[d]);
+    return true;
+  };
+#pragma clang loop unroll(disable)
+  for (int i = 0; i < n; i += kDepth) {
+    if (!group(i, std::integral_constant<int, 0>{}) || !group(i, std::integral_constant<int, 1>{})) break;
+    if constexpr (kDepth > 2) {
+      if (!group(i, std::integral_constant<int, 2>{})) break;
+    }
+    if constexpr (kDepth > 3) {
+      if (!group(i, std::integral_constant<int, 3>{})) break;
+    }
   }
 }
 
@@ -470,7 +512,8 @@ int resident_workgroups(const void* kernel, int threads, int slot, hipStream_t s
 namespace {
 
 // Workgroups of the bf16 decode grid at most (four workers each): what 256
-// compute units hold at four waves per SIMD. The workspace is sized for it.
+// compute units hold at four waves per SIMD (the kernel runs two). The
+// workspace is sized for it.
 constexpr int kMaxDecodeGrid = 1024;
 
 template <int G>
