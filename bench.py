@@ -45,10 +45,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 5093760.9, 25491.8),
-    "llama3-8b-decode": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 463938.6, 9332.6),
-    "llama3-8b-mixed-step": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 1152544.9, 10362.9),
-    "llama3-8b-pressure": ("bd76aa0348ee7d4fc8ff7f604745d394a723509d5ca0f542264f9a929eeb50f6", 622034.6, 15235.7),
+    "llama3-70b-decode": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 4996952.0, 16491.3),
+    "llama3-8b-decode": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 455811.9, 5174.1),
+    "llama3-8b-mixed-step": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 1131361.9, 6151.3),
+    "llama3-8b-pressure": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 609531.9, 10093.4),
 }
 
 
