@@ -177,10 +177,17 @@ int bros_attn_decode(void* out, const void* q,
  *   max_q_len    : host-side upper bound of every n (sizes the grid)
  *   max_ctx      : host-side upper bound of every ctx_lens[s]
  *   workspace    : at least bros_attn_workspace_size(BROS_WS_PREFILL, dtype,
- *                  num_q_tokens, num_q_heads, head_dim, max_ctx) bytes.
+ *                  num_q_tokens, num_q_heads, head_dim, max_ctx) bytes,
+ *                  16-byte aligned; owned by the caller, contents undefined
+ *                  after the call.
  * bf16 runs the QK^T and PV products on the matrix cores (P is rounded to bf16
- * before PV) for max_ctx <= 32768; fp32, and bf16 beyond that context, run a
- * vector-ALU path that needs the workspace the size query reports.
+ * before PV) for max_ctx <= 32768. There the workspace is optional (NULL, or
+ * one smaller than the query, is accepted): with it, when the call's (row
+ * tile, KV head) units are fewer than the compute units, long units are split
+ * over key ranges whose partial results are merged, so idle compute units
+ * take a share; without it every unit runs whole. The merged rows differ from
+ * the unsplit ones by rounding only. fp32, and bf16 beyond that context, run
+ * a vector-ALU path that requires the workspace (BROS_E_WORKSPACE otherwise).
  */
 int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
                             int32_t num_q_tokens, int32_t max_q_len,

@@ -91,7 +91,8 @@ size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
   const bool bf16 = dtype == BROS_BF16;
   if (kind == BROS_WS_DECODE) return bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx, bf16);
   if (kind == BROS_WS_PREFILL)
-    return (bf16 && max_ctx <= bros::kPrefillMaxCtxMfma) ? 0 : bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx, bf16);
+    return (bf16 && max_ctx <= bros::kPrefillMaxCtxMfma) ? bros::prefill_workspace_bytes()
+                                                          : bros::decode_workspace_bytes(num_rows, num_q_heads, max_ctx, bf16);
   return 0;
 }
 
@@ -181,7 +182,7 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
     a.block_tables = block_tables;
     a.dir = dir;
     a.cls = cls;
-  a.dir_per_entry = dir_per_entry;
+    a.dir_per_entry = dir_per_entry;
     a.ctx_lens = ctx_lens;
     a.num_q_tokens = num_q_tokens;
     a.num_seqs = num_seqs;
@@ -194,7 +195,9 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
     a.tiles_per_seq = (max_q_len + qt - 1) / qt;
     a.scale_log2 = scale_log2;
     const long long total = (long long)num_seqs * num_kv_heads * a.tiles_per_seq;
-    if (total > 0x7fffffffLL) return fail(BROS_E_SHAPE, "%s: grid of %lld workgroups too large", fn, total);
+    if (total > 0x7fffffffLL - 1024) return fail(BROS_E_SHAPE, "%s: grid of %lld workgroups too large", fn, total);
+    // the workspace is optional here: with one of the queried size, long units are split
+    if (aligned(workspace, 16)) bros::set_prefill_workspace(a, workspace, workspace_bytes);
     return launch_status(fn, bros::launch_prefill_mfma(a, group, (int)total, s));
   }
 

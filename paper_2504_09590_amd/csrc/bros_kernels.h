@@ -79,6 +79,16 @@ struct PrefillArgs {
   int32_t num_kv_heads;
   int32_t tiles_per_seq;  // ceil(max_q_len / positions per tile)
   float scale_log2;
+  // Splitting long units into pieces over key ranges (none when num_cus is 0):
+  // the compute units the work is spread over, the partials of split units,
+  // [ws_slots][128 rows] x (ws_o: 128 dims, ws_ml: max and sum) in fp32, and
+  // the list of split units that the merge walks (count, then (item, parts,
+  // first slot) triples).
+  int32_t num_cus;
+  int32_t ws_slots;
+  float* ws_o;
+  float* ws_ml;
+  int32_t* ws_list;
 };
 
 // Rows of a list of slots moved between the pool and a dense [n][Hkv][D]
@@ -112,7 +122,19 @@ hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream)
 // Longest context the matrix-core prefill handles (its block table is staged
 // whole in LDS); longer contexts take the vector path.
 constexpr int32_t kPrefillMaxCtxMfma = 32768;
-hipError_t launch_prefill_mfma(const PrefillArgs& a, int group, int num_tiles_total, hipStream_t stream);
+// Compute units enabled for `stream` (a stream made with
+// hipExtStreamCreateWithCUMask runs on a subset of the device): the device's
+// count is queried once per device, the stream's CU mask read on every call.
+int stream_compute_units(hipStream_t stream);
+// Workgroups of `kernel` (launched with `threads` threads) that the compute
+// units enabled for `stream` hold at once; the per-CU occupancy is queried once
+// per device and cache slot (0..7: bf16 decode 0..3, fp32 decode 4..7).
+int resident_workgroups(const void* kernel, int threads, int slot, hipStream_t stream);
+
+hipError_t launch_prefill_mfma(PrefillArgs a, int group, int num_tiles_total, hipStream_t stream);
 int prefill_positions_per_tile(int group);
+// Workspace of the matrix-core prefill (optional: without it no unit is split).
+size_t prefill_workspace_bytes();
+void set_prefill_workspace(PrefillArgs& a, void* ws, size_t bytes);
 
 }  // namespace bros

@@ -482,15 +482,33 @@ int stream_cus(hipStream_t stream, int fallback) {
 
 }  // namespace
 
+int stream_compute_units(hipStream_t stream) {
+  constexpr int kMaxDevices = 64;
+  static int cus_cache[kMaxDevices];
+  static std::mutex mu;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int cus = 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (cus_cache[dev] == 0) {
+      int n = 0;
+      if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+      cus_cache[dev] = n;
+    }
+    cus = cus_cache[dev];
+  }
+  return stream_cus(stream, cus);
+}
+
 int resident_workgroups(const void* kernel, int threads, int slot, hipStream_t stream) {
   constexpr int kMaxDevices = 64;
   constexpr int kSlots = 8;
   static int per_cu_cache[kMaxDevices][kSlots];
-  static int cus_cache[kMaxDevices];
   static std::mutex mu;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 1024;
-  int per_cu = 0, cus = 0;
+  int per_cu = 0;
   {
     std::lock_guard<std::mutex> lock(mu);
     if (per_cu_cache[dev][slot] == 0) {
@@ -498,15 +516,9 @@ int resident_workgroups(const void* kernel, int threads, int slot, hipStream_t s
       if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n <= 0) n = 4;
       per_cu_cache[dev][slot] = n;
     }
-    if (cus_cache[dev] == 0) {
-      int n = 0;
-      if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-      cus_cache[dev] = n;
-    }
     per_cu = per_cu_cache[dev][slot];
-    cus = cus_cache[dev];
   }
-  return per_cu * stream_cus(stream, cus);
+  return per_cu * stream_compute_units(stream);
 }
 
 namespace {

@@ -58,13 +58,6 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Workgroups of `kernel` (launched with `threads` threads) that the compute
-// units enabled for `stream` hold at once: the per-CU occupancy is queried
-// once per device and cache slot, the CU count is read from the stream's CU
-// mask on every call (a stream made with hipExtStreamCreateWithCUMask runs on
-// a subset of the device).
-int resident_workgroups(const void* kernel, int threads, int slot, hipStream_t stream);
-
 hipError_t launch_decode_f32(const DecodeArgs& a, int group, hipStream_t stream);
 
 }  // namespace bros

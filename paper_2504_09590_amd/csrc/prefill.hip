@@ -13,13 +13,19 @@
 // wave's vector work (the softmax) runs beside the other's matrix-core
 // products -- a single wave issues vector instructions at about half the rate
 // two waves reach -- and one unit's start-up (lengths, Q, first tiles) hides
-// behind the other's steps. (With kHalves = 2 the kernel instead runs 8 waves
-// per workgroup that split the key tiles in two halves merged through LDS at
-// the end, one workgroup per unit and per compute unit; on MI355X that is
-// about 10 % slower.)
-// Workgroups are launched longest unit first (ranked on the device from the
-// length table), and consecutive ids are spread over the XCDs so that one KV
-// head of every sequence stays on one XCD's L2.
+// behind the other's steps.
+//
+// Balance. All units of a step usually run in one round, so the kernel lasts
+// as long as its longest unit. When the units are fewer than the compute
+// units (a long context under few chunk rows) and a workspace is given, a
+// unit whose key tiles exceed the part size T is split into ceil(tiles / T)
+// pieces over disjoint key ranges, T = ceil(all tiles x Hkv / compute units)
+// (at least kMinPartTiles). A split unit's pieces write unnormalised partial
+// rows with their max and sum; prefill_merge_kernel folds them (the same
+// max-rescaled sum as the decode's merge). Unsplit units write their rows
+// directly. Units (or pieces) are launched longest first, ranked on the device
+// from the length table, and consecutive ids are spread over the XCDs so that
+// one KV head of every sequence stays on one XCD's L2.
 //
 // Data path. K and V rows go straight from the pool into LDS
 // (global_load_lds, no registers), row-major [key][d] with the 16-byte chunks
@@ -63,11 +69,7 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 
-// Key halves per workgroup: 2 = 8 waves (two per SIMD) splitting a unit's key
-// tiles between two wave sets; 1 = 4 waves (one per SIMD) each taking all of
-// its rows' key tiles, two workgroups sharing a compute unit.
-constexpr int kHalves = 1;
-constexpr int kThreads = 256 * kHalves;
+constexpr int kThreads = 256;                      // 4 waves: one per SIMD, two workgroups per CU
 constexpr int kRows = 128;                         // query rows per workgroup
 constexpr int kKeys = 32;                          // keys per tile (2 blocks)
 constexpr int kSlots = 4;                          // stages of the K ring and of the V ring
@@ -76,7 +78,9 @@ constexpr int kTileBytes = kKeys * kRowBytes;      // one K or V tile in LDS
 constexpr float kRescaleSlack = 8.0f;              // log2 units
 constexpr float kNoMax = -1.0e30f;
 constexpr int kMaxTableLds = kPrefillMaxCtxMfma / kBlockSize;   // table entries staged in LDS
-constexpr int kMaxRankItems = kThreads;            // units ranked by length on the device
+constexpr int kMaxRankItems = kThreads;            // units planned on the device (one per thread)
+constexpr int kMaxPieces = 2 * kThreads;           // pieces ranked on the device (two per thread)
+constexpr int kMinPartTiles = 8;                   // the shortest piece a unit is split into
 constexpr int kLoadsPerStep = 4;                   // two K and two V loads per wave per step
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(v4u_t v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -152,72 +156,199 @@ __device__ __forceinline__ int unit_tiles(const PrefillArgs& a, int s, int t, in
   return (kend + kKeys - 1) / kKeys;
 }
 
+// Inclusive prefix sum of v over the workgroup's threads (thread order);
+// *total gets the sum. `scratch` holds kThreads / kWave ints. Every thread
+// of the workgroup calls it.
+__device__ int block_scan(int v, int* scratch, int* total) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x / kWave;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int u = __shfl_up(v, o);
+    if (lane >= o) v += u;
+  }
+  if (lane == kWave - 1) scratch[w] = v;
+  __syncthreads();
+  int before = 0, sum = 0;
+#pragma unroll
+  for (int i = 0; i < kThreads / kWave; ++i) {
+    const int x = scratch[i];
+    before += i < w ? x : 0;
+    sum += x;
+  }
+  __syncthreads();
+  *total = sum;
+  return v + before;
+}
+
+// Index of the entry of rank `rank` among len[0 .. n), longest first (ties
+// by index), or -1 past the last. len is 16-byte aligned LDS, padded with -1
+// up to a multiple of 4 entries; s_res is one int of LDS. Every thread of the
+// workgroup calls it; the result is uniform.
+__device__ int find_rank(const int* len, int n, int rank, int* s_res) {
+  const int tid = threadIdx.x;
+  if (tid == 0) *s_res = -1;
+  __syncthreads();
+  const int n4 = (n + 3) / 4;
+  for (int k = tid; k < n; k += kThreads) {
+    const int my = len[k];
+    int r = 0;
+    int j4 = 0;
+    for (; j4 + 4 <= n4; j4 += 4) {   // four reads in flight
+      int4 l4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) l4[u] = reinterpret_cast<const int4*>(len)[j4 + u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int lj[4] = {l4[u].x, l4[u].y, l4[u].z, l4[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r += (lj[e] > my) | ((lj[e] == my) & (4 * (j4 + u) + e < k));
+      }
+    }
+    for (; j4 < n4; ++j4) {
+      const int4 l4 = reinterpret_cast<const int4*>(len)[j4];
+      const int lj[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) r += (lj[e] > my) | ((lj[e] == my) & (4 * j4 + e < k));
+    }
+    if (r == rank) *s_res = k;
+  }
+  __syncthreads();
+  return __builtin_amdgcn_readfirstlane(*s_res);
+}
+
+// What a workgroup of the prefill grid works on: key tiles
+// [part L / parts, (part + 1) L / parts) of unit (item, KV head), L being the
+// unit's key tiles. Split units (parts > 1) keep their partial rows in
+// workspace slots first_slot .. first_slot + parts - 1 (times Hkv).
+struct PiecePlan {
+  int item;         // -1: nothing for this rank
+  int part;
+  int parts;
+  int first_slot;
+};
+
+// The piece of rank `rank` (longest first). Items are (sequence, tile of
+// positions); all KV heads of an item have its length L (key tiles of its
+// last row). Without splitting (num_cus 0) each item is one piece. With it,
+// the part size is T = max(kMinPartTiles, ceil(sum L x Hkv / num_cus)), the
+// mean work of a compute unit, and an item becomes ceil(L / T) pieces; then
+// ranks exceed the items by at most num_cus / Hkv and split pieces times Hkv
+// number at most 2 num_cus. Workgroup 0 writes the list of split items for
+// the merge. `scratch` is 2 kMaxPieces + 4 + kThreads / kWave ints of LDS,
+// 16-byte aligned, that nothing else uses meanwhile. Every thread of the
+// workgroup calls it.
+template <int QT>
+__device__ PiecePlan plan_pieces(const PrefillArgs& a, int rank, int* scratch) {
+  const int tid = threadIdx.x;
+  const int tps = a.tiles_per_seq;
+  const int n_items = a.num_seqs * tps;
+  if (n_items > kMaxRankItems) {
+    // (never split) the longest tile of every sequence first
+    const int t_rank = rank / a.num_seqs;
+    return PiecePlan{t_rank < tps ? (rank % a.num_seqs) * tps + (tps - 1 - t_rank) : -1, 0, 1, 0};
+  }
+  int* s_len = scratch;                     // [kMaxPieces] lengths, then -1 padding
+  int* s_pid = scratch + kMaxPieces;        // [kMaxPieces] item * 1024 + part
+  int* s_res = scratch + 2 * kMaxPieces;    // [4]
+  int* s_red = s_res + 4;                   // [kThreads / kWave]
+  const int L = tid < n_items ? unit_tiles(a, tid / tps, tid % tps, QT) : -1;
+  int P = 1, n_pieces = n_items, pbase = tid, sbase = 0;
+  bool split = false;
+  if (a.num_cus > 0) {
+    int total = 0;
+    block_scan(max(L, 0), s_red, &total);
+    const int T = max(kMinPartTiles, (int)(((int64_t)total * a.num_kv_heads + a.num_cus - 1) / a.num_cus));
+    const int Pt = L > 0 ? 1 + (L - 1) / T : 0;
+    const int pend = block_scan(Pt, s_red, &n_pieces);
+    const int own = Pt > 1 ? Pt : 0;
+    int n_split = 0;
+    const int send = block_scan(own, s_red, &n_split);
+    split = n_split > 0 && n_pieces <= kMaxPieces && (int64_t)n_split * a.num_kv_heads <= a.ws_slots;
+    if (split) {
+      P = Pt;
+      pbase = pend - Pt;
+      sbase = send - own;
+    } else {
+      n_pieces = n_items;
+    }
+    if (blockIdx.x == 0) {
+      // the split items, in item order: count, then (item, parts, first slot)
+      int count = 0;
+      const int is = split && P > 1 ? 1 : 0;
+      const int idx = block_scan(is, s_red, &count) - is;
+      if (is) {
+        a.ws_list[1 + 3 * idx] = tid;
+        a.ws_list[2 + 3 * idx] = P;
+        a.ws_list[3 + 3 * idx] = sbase;
+      }
+      if (tid == 0) a.ws_list[0] = split ? count : 0;
+    }
+  }
+  if (!split) {
+    if (tid < kMaxRankItems) s_len[tid] = L;   // -1 past the items
+    const int k = find_rank(s_len, n_items, rank, s_res);
+    __syncthreads();   // the scratch is the caller's again
+    return PiecePlan{k, 0, 1, 0};
+  }
+  if (tid < n_items) {
+    for (int q = 0; q < P; ++q) {
+      s_len[pbase + q] = (int)((int64_t)(q + 1) * L / P) - (int)((int64_t)q * L / P);
+      s_pid[pbase + q] = tid * 1024 + q;
+    }
+  }
+  if (tid < ((n_pieces + 3) & ~3) - n_pieces) s_len[n_pieces + tid] = -1;   // padding
+  const int k = find_rank(s_len, n_pieces, rank, s_res);
+  PiecePlan out{-1, 0, 0, 0};
+  if (k >= 0) {
+    const int id = s_pid[k];
+    const int item = id / 1024;
+    if (tid == item) {
+      s_res[1] = P;
+      s_res[2] = sbase;
+    }
+    __syncthreads();
+    out = PiecePlan{item, id % 1024, s_res[1], s_res[2]};
+  }
+  __syncthreads();   // the scratch is the caller's again
+  return out;
+}
+
 template <int G>
-__global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a) {
   constexpr int QT = kRows / G;   // positions per unit
   // K ring and V ring, kSlots slots each; a slot holds the even-tile half and
   // the odd-tile half (kTileBytes each). Slot offsets are compile-time
   // constants below 64 KiB, so they fold into the LDS instructions' offset
   // field.
-  constexpr int kSlotBytes = kHalves * kTileBytes;
+  constexpr int kSlotBytes = kTileBytes;
   __shared__ __attribute__((aligned(1024))) uint8_t s_kring[kSlots * kSlotBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t s_vring[kSlots * kSlotBytes];
   __shared__ int s_first_bad;
   __shared__ int s_tbl[kMaxTableLds];   // the sequence's validated table entries (-1: invalid)
   __shared__ int8_t s_dir[kMaxTableLds];   // each entry's direction (+1 / -1)
-  __shared__ __attribute__((aligned(16))) int s_len[kMaxRankItems];
-  __shared__ int s_item;
+
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wv = wave_id_uniform();
   const int rg = wv & 3;    // row group: rows 32 rg .. 32 rg + 31
-  const int kh = kHalves == 2 ? (wv >> 2) : 0;   // key half: tiles kh, kh + kHalves, ...
 
-  // ---- Which unit: rank by key tiles, longest first (ties by index). Ids
+  // ---- Which piece: rank by key tiles, longest first (ties by index). Ids
   // r * Hkv + g give every rank all KV heads on consecutive ids, i.e. on
   // different XCDs (id % 8), and one KV head of every unit on one XCD when
   // Hkv is a multiple of 8.
   const int Hkv = a.num_kv_heads;
   const int tps = a.tiles_per_seq;
-  const int n_items = a.num_seqs * tps;
   const int g = blockIdx.x % Hkv;
   const int rank = blockIdx.x / Hkv;
-  int item;
-  if (n_items <= kMaxRankItems) {
-    int my_len = -1;   // the padding entries never outrank a unit
-    if (tid < n_items) my_len = unit_tiles(a, tid / tps, tid % tps, QT);
-    s_len[tid] = my_len;
-    __syncthreads();
-    if (tid < n_items) {
-      int r = 0;
-      const int n4 = (n_items + 3) / 4;
-      int j4 = 0;
-      for (; j4 + 4 <= n4; j4 += 4) {   // four reads in flight
-        int4 l4[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) l4[u] = reinterpret_cast<const int4*>(s_len)[j4 + u];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int lj[4] = {l4[u].x, l4[u].y, l4[u].z, l4[u].w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) r += (lj[e] > my_len) | ((lj[e] == my_len) & (4 * (j4 + u) + e < tid));
-        }
-      }
-      for (; j4 < n4; ++j4) {
-        const int4 l4 = reinterpret_cast<const int4*>(s_len)[j4];
-        const int lj[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) r += (lj[e] > my_len) | ((lj[e] == my_len) & (4 * j4 + e < tid));
-      }
-      if (r == rank) s_item = tid;
-    }
-    __syncthreads();
-    item = __builtin_amdgcn_readfirstlane(s_item);
-  } else {
-    // longest tile of every sequence first
-    item = (rank % a.num_seqs) * tps + (tps - 1 - rank / a.num_seqs);
-  }
+  // (the K ring is free until the first loads)
+  const PiecePlan plan = plan_pieces<QT>(a, rank, reinterpret_cast<int*>(s_kring));
+  const int item = __builtin_amdgcn_readfirstlane(plan.item);
+  if (item < 0) return;                      // a rank past the last piece
+  const int part = __builtin_amdgcn_readfirstlane(plan.part);
+  const int parts = __builtin_amdgcn_readfirstlane(plan.parts);
+  const int pslot = __builtin_amdgcn_readfirstlane(plan.first_slot);
   const int s = item / tps;
   const int t = item % tps;
 
@@ -230,13 +361,16 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
   const int c0 = ctx_s - n;
   const int ctx = min(ctx_s, min(a.max_ctx, a.max_blocks_per_seq * kBlockSize));
   const int kend = min(ctx, c0 + min(n, t0 + QT));
-  const int n_kt = (kend + kKeys - 1) / kKeys;   // key tiles of the unit
-  if (n_kt == 0) return;
+  const int unit_kt = (kend + kKeys - 1) / kKeys;   // key tiles of the unit
+  // this piece's key tiles [kb, kb + n_kt)
+  const int kb = (int)((int64_t)part * unit_kt / parts);
+  const int n_kt = (int)((int64_t)(part + 1) * unit_kt / parts) - kb;
+  if (n_kt <= 0) return;
   const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
   // keys below this logical position are visible to every row of the unit
   const int full_below = min(ctx, c0 + t0 + 1);
-  const int n_steps = (n_kt + kHalves - 1) / kHalves;        // both halves step together
-  const int n_mine = (n_kt - kh + kHalves - 1) / kHalves;     // tiles of this wave's half
+  const int n_steps = n_kt;   // one tile per step
+  const int n_mine = n_kt;
 
   const int half = lane >> 5;
   const int mrow = lane & 31;
@@ -262,9 +396,9 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
   }
 
   // Table entries come in as scalar loads (block b of the sequence, or -1
-  // for an entry past the context or out of range). The tile of step j for
-  // this wave's half is 2 j + kh; this wave loads, positions and fixes up
-  // rows 8 rg .. 8 rg + 7 of it, in block rg / 2.
+  // for an entry past the context or out of range). The tile of step j is
+  // kb + j; this wave loads, positions and fixes up rows 8 rg .. 8 rg + 7 of
+  // it, in block rg / 2.
   const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
   const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
   const int32_t* tbl = a.block_tables + (size_t)s * a.max_blocks_per_seq;
@@ -278,7 +412,7 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
   // Read a step ahead of its use; the value comes back in a vector register
   // and is made scalar where it is used.
   auto own = [&](int j) -> int {
-    const int b = 2 * (kHalves * j + kh) + my_bt;
+    const int b = 2 * (kb + j) + my_bt;
     return b < nblk ? s_tbl[b] : -1;
   };
   auto valid = [&](int j, int v) -> int { return __builtin_amdgcn_readfirstlane(v); };
@@ -297,21 +431,20 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
   }
   auto issue = [&](int j, int raw, const uint16_t* pool, uint8_t* ring) __attribute__((always_inline)) {
     const int blk = valid(j, raw);
-    const int b = (kHalves * j + kh < n_kt && blk >= 0) ? blk : 0;
+    const int b = (j < n_kt && blk >= 0) ? blk : 0;
     const uint16_t* base = pool + ((size_t)b * Hkv + g) * kBlockSize * kHeadDim;
-    uint8_t* dst = ring + kh * kTileBytes + 8 * rg * kRowBytes;
+    uint8_t* dst = ring + 8 * rg * kRowBytes;
 #pragma unroll
     for (int i = 0; i < 2; ++i) load_to_lds(base, ld_off[i], dst + 4 * i * kRowBytes);
   };
   // Once this wave's V loads of step j have landed: zero its rows whose slot
   // is not context.
   auto fixup_v = [&](int j, int raw, uint8_t* ring) __attribute__((always_inline)) {
-    const int tile = kHalves * j + kh;
-    if (tile >= n_kt) return;
+    if (j >= n_kt) return;
     const int blk = valid(j, raw);
-    const int b = 2 * tile + my_bt;
+    const int b = 2 * (kb + j) + my_bt;
     if (blk >= 0 && (b + 1) * kBlockSize <= ctx) return;
-    uint8_t* dv = ring + kh * kTileBytes + 8 * rg * kRowBytes;
+    uint8_t* dv = ring + 8 * rg * kRowBytes;
     const int dirv = s_dir[b < nblk ? b : 0];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
@@ -482,8 +615,8 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
     issue(ii + 5, eK, kpool, s_kring + sl1 * kSlotBytes);
     issue(ii + 4, eV, vpool, s_vring + sl * kSlotBytes);
   };
-  const uint8_t* kr = s_kring + kh * kTileBytes;
-  const uint8_t* vr = s_vring + kh * kTileBytes;
+  const uint8_t* kr = s_kring;
+  const uint8_t* vr = s_vring;
 
   // ---- Prologue. Step j's K tile lives in K slot j % 4, its V tile in V
   // slot j % 4. Batch b = (K of step
@@ -492,7 +625,7 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
   // the first scores are in. Table entries run ahead of their use in a
   // window: w0 .. w4 hold this wave's entries for steps ii + 1 .. ii + 5.
   // (the first entries as scalar loads: the LDS copy is made while they load)
-  auto own0 = [&](int j) -> int { return entry(2 * (kHalves * j + kh) + my_bt); };
+  auto own0 = [&](int j) -> int { return entry(2 * (kb + j) + my_bt); };
   const int e0 = own0(0);
   int w0 = own0(1), w1 = own0(2), w2 = own0(3), w3 = own0(4), w4 = own0(5);
   issue(0, e0, kpool, s_kring);
@@ -523,8 +656,8 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
     v4u_t kv[8];
     k_operands(kr, kv);
     scores(kv, sa);
-    if (kh >= plain_tiles) mask_max(sa, std::true_type{}, kh);
-    else mask_max(sa, std::false_type{}, kh);
+    if (kb >= plain_tiles) mask_max(sa, std::true_type{}, kb);
+    else mask_max(sa, std::false_type{}, kb);
   }
   lds_barrier();   // K slot 0 is free again
   issue(2, w1, kpool, s_kring + 2 * kSlotBytes);
@@ -550,8 +683,8 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
     w3 = w4;
     w4 = nw;
   };
-  // this wave's tiles 2 j + kh below plain_tiles, as a step bound
-  const int n_plain = min(n_mine, (plain_tiles - kh + kHalves - 1) / kHalves);
+  // the piece's tiles below plain_tiles, as a step bound
+  const int n_plain = max(0, min(n_mine, plain_tiles - kb));
   auto main_step = [&](auto uc) __attribute__((always_inline)) -> bool {
     constexpr int u = decltype(uc)::value;
     if (ii + 1 >= n_plain) return false;
@@ -575,8 +708,7 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
     const int sl = ii & (kSlots - 1);
     const int sl1 = (sl + 1) & (kSlots - 1);
     const int nw = own(ii + 6);
-    step(kr + sl1 * kSlotBytes, vr + sl * kSlotBytes, kHalves * (ii + 1) + kh, std::true_type{}, std::true_type{}, sa,
-         sb);
+    step(kr + sl1 * kSlotBytes, vr + sl * kSlotBytes, kb + ii + 1, std::true_type{}, std::true_type{}, sa, sb);
     sa = sb;
     rescale_o();
     advance(ii, sl, w0, w3, w4, std::true_type{});
@@ -599,85 +731,163 @@ __global__ __launch_bounds__(kThreads, 2 / kHalves) void prefill_mfma_kernel(Pre
   }
 
   wait_vmem<0>();
-  if constexpr (kHalves == 1) {
-    // ---- One key set: normalise and write the rows.
-    l_run = pair_sum(l_run);
-    const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
-    if (row_valid) {
-      uint16_t* op = static_cast<uint16_t*>(a.out) + row_off;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-#pragma unroll
-        for (int jq = 0; jq < 4; ++jq) {
-          const int d0 = 32 * dt + 8 * jq + 4 * half;   // accumulators 4jq..4jq+3 are dims d0..d0+3
-          uint2 w;
-          w.x = pack2_bf16(o[dt][4 * jq + 0] * inv, o[dt][4 * jq + 1] * inv);
-          w.y = pack2_bf16(o[dt][4 * jq + 2] * inv, o[dt][4 * jq + 3] * inv);
-          *reinterpret_cast<uint2*>(op + d0) = w;
-        }
-      }
-    }
-    return;
-  } else {
-  // ---- Merge the two key halves through LDS (K ring reused once every load
-  // has landed and every wave is past the last step) and write the rows.
-  lds_barrier();
   l_run = pair_sum(l_run);
-  float* xo = reinterpret_cast<float*>(s_kring + rg * kSlotBytes);   // per row group: [dt][jq][lane] float4 = 16 KB
-  float* xm = reinterpret_cast<float*>(s_vring);                     // [rg][m, l][lane]
-  if (kh == 1) {
+  if (parts > 1) {
+    // ---- A piece of a split unit: unnormalised rows plus their max and sum.
+    const size_t slot = ((size_t)(pslot + part) * Hkv + g) * kRows + r_unit;
+    float* po = a.ws_o + slot * kHeadDim;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+    for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        const float4 v = make_float4(o[dt][4 * jq], o[dt][4 * jq + 1], o[dt][4 * jq + 2], o[dt][4 * jq + 3]);
-        *reinterpret_cast<float4*>(xo + ((dt * 4 + jq) * kWave + lane) * 4) = v;
+        const int d0 = 32 * dt + 8 * jq + 4 * half;   // accumulators 4jq..4jq+3 are dims d0..d0+3
+        *reinterpret_cast<float4*>(po + d0) =
+            make_float4(o[dt][4 * jq], o[dt][4 * jq + 1], o[dt][4 * jq + 2], o[dt][4 * jq + 3]);
       }
-    xm[(rg * 2 + 0) * kWave + lane] = m_run;
-    xm[(rg * 2 + 1) * kWave + lane] = l_run;
+    }
+    if (half == 0) {
+      a.ws_ml[2 * slot] = m_run;
+      a.ws_ml[2 * slot + 1] = l_run;
+    }
+    return;
   }
-  lds_barrier();
-  if (kh == 0) {
-    const float m1x = xm[(rg * 2 + 0) * kWave + lane];
-    const float l1 = xm[(rg * 2 + 1) * kWave + lane];
-    const float m = fmaxf(m_run, m1x);
-    const float wt0 = fast_exp2(m_run - m), wt1 = fast_exp2(m1x - m);
-    const float l = l_run * wt0 + l1 * wt1;
-    const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-    const float f0 = wt0 * inv, f1 = wt1 * inv;
-    if (row_valid) {
-      uint16_t* op = static_cast<uint16_t*>(a.out) + row_off;
+  // ---- A whole unit: normalise and write the rows.
+  const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+  if (row_valid) {
+    uint16_t* op = static_cast<uint16_t*>(a.out) + row_off;
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
+    for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
-        for (int jq = 0; jq < 4; ++jq) {
-          const float4 v1 = *reinterpret_cast<const float4*>(xo + ((dt * 4 + jq) * kWave + lane) * 4);
-          const int d0 = 32 * dt + 8 * jq + 4 * half;   // accumulators 4jq..4jq+3 are dims d0..d0+3
-          uint2 w;
-          w.x = pack2_bf16(o[dt][4 * jq + 0] * f0 + v1.x * f1, o[dt][4 * jq + 1] * f0 + v1.y * f1);
-          w.y = pack2_bf16(o[dt][4 * jq + 2] * f0 + v1.z * f1, o[dt][4 * jq + 3] * f0 + v1.w * f1);
-          *reinterpret_cast<uint2*>(op + d0) = w;
-        }
+      for (int jq = 0; jq < 4; ++jq) {
+        const int d0 = 32 * dt + 8 * jq + 4 * half;   // accumulators 4jq..4jq+3 are dims d0..d0+3
+        uint2 w;
+        w.x = pack2_bf16(o[dt][4 * jq + 0] * inv, o[dt][4 * jq + 1] * inv);
+        w.y = pack2_bf16(o[dt][4 * jq + 2] * inv, o[dt][4 * jq + 3] * inv);
+        *reinterpret_cast<uint2*>(op + d0) = w;
       }
     }
   }
+}
+
+// Fold the pieces of split units: one workgroup per (split item, KV head),
+// from the list the prefill grid's first workgroup wrote. Per row, with
+// M = max_p m_p (log2 units): o = sum_p 2^(m_p - M) O_p / sum_p 2^(m_p - M) l_p.
+// Rows of unsplit units were written by the prefill kernel itself.
+template <int G>
+__global__ __launch_bounds__(kThreads) void prefill_merge_kernel(PrefillArgs a) {
+  constexpr int QT = kRows / G;
+  __shared__ float s_m[kRows];
+  __shared__ float s_inv[kRows];
+  const int Hkv = a.num_kv_heads;
+  const int j = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
+  if (j >= load_uniform(a.ws_list, 0)) return;
+  const int item = load_uniform(a.ws_list, 1 + 3 * j);
+  const int parts = load_uniform(a.ws_list, 2 + 3 * j);
+  const int slot0 = load_uniform(a.ws_list, 3 + 3 * j);
+  const int tps = a.tiles_per_seq;
+  const int s = item / tps, t = item % tps;
+  const int q_begin = load_uniform(a.cu_q, s);
+  const int n = load_uniform(a.cu_q, s + 1) - q_begin;
+  if (q_begin < 0 || n <= 0 || q_begin + n > a.num_q_tokens || t * QT >= n) return;   // (never split)
+  const size_t row0 = ((size_t)slot0 * Hkv + g) * kRows;   // workspace row of part 0, unit row 0
+  const size_t pstride = (size_t)Hkv * kRows;              // workspace rows from one part to the next
+  const int tid = threadIdx.x;
+  if (tid < kRows) {
+    float m = -INFINITY;
+    for (int p = 0; p < parts; ++p) m = fmaxf(m, a.ws_ml[2 * (row0 + p * pstride + tid)]);
+    float l = 0.0f;
+    for (int p = 0; p < parts; ++p) {
+      const size_t row = row0 + p * pstride + tid;
+      l = fmaf(a.ws_ml[2 * row + 1], fast_exp2(a.ws_ml[2 * row] - m), l);
+    }
+    s_m[tid] = m;
+    s_inv[tid] = l > 0.0f ? 1.0f / l : 0.0f;
   }
+  __syncthreads();
+  const int c4 = tid & 31;   // dims 4 c4 .. 4 c4 + 3 of rows tid / 32 + 8 i
+#pragma unroll 2
+  for (int i = 0; i < kRows / 8; ++i) {
+    const int r = 8 * i + (tid >> 5);
+    const int qrow = t * QT + r % QT;
+    if (qrow >= n) continue;
+    const float m = s_m[r];
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int p = 0; p < parts; ++p) {
+      const size_t row = row0 + p * pstride + r;
+      const float w = fast_exp2(a.ws_ml[2 * row] - m);
+      const float4 v = reinterpret_cast<const float4*>(a.ws_o + row * kHeadDim)[c4];
+      acc.x = fmaf(v.x, w, acc.x);
+      acc.y = fmaf(v.y, w, acc.y);
+      acc.z = fmaf(v.z, w, acc.z);
+      acc.w = fmaf(v.w, w, acc.w);
+    }
+    const float inv = s_inv[r];
+    uint2 o2;
+    o2.x = pack2_bf16(acc.x * inv, acc.y * inv);
+    o2.y = pack2_bf16(acc.z * inv, acc.w * inv);
+    const size_t orow = (size_t)(q_begin + qrow) * a.num_q_heads + g * G + r / QT;
+    reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + orow * kHeadDim)[c4] = o2;
+  }
+}
+
+// Compute units a split plan spreads over, at most; the workspace holds
+// 2 x this many (split piece, KV head) partials.
+constexpr int kMaxPrefillCus = 512;
+
+template <int G>
+hipError_t launch_group(PrefillArgs a, int num_units, hipStream_t stream) {
+  // Split only when the units leave compute units idle: with a unit or more
+  // per compute unit, splitting measured no faster (its partials and merge
+  // cost what the better balance saves).
+  a.num_cus = 0;
+  if (a.ws_o != nullptr && num_units / a.num_kv_heads <= kMaxRankItems) {
+    int cus = stream_compute_units(stream);
+    cus = cus < kMaxPrefillCus ? cus : kMaxPrefillCus;
+    if (num_units < cus) a.num_cus = cus;
+  }
+  // ranks beyond the units: at most num_cus / Hkv more pieces than items
+  const long long grid = (long long)num_units + a.num_cus;
+  hipLaunchKernelGGL(prefill_mfma_kernel<G>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.num_cus == 0) return e;
+  // split items x Hkv <= num_cus
+  hipLaunchKernelGGL(prefill_merge_kernel<G>, dim3((unsigned)a.num_cus), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 int prefill_positions_per_tile(int group) { return kRows / group; }
 
-hipError_t launch_prefill_mfma(const PrefillArgs& a, int group, int num_tiles_total, hipStream_t stream) {
+size_t prefill_workspace_bytes() {
+  const size_t rows = 2 * (size_t)kMaxPrefillCus * kRows;   // (split piece, KV head) partials x rows
+  const size_t bytes = rows * kHeadDim * sizeof(float) + rows * 2 * sizeof(float) + (1 + 3 * (size_t)kMaxRankItems) * sizeof(int32_t);
+  return (bytes + 255) & ~(size_t)255;
+}
+
+void set_prefill_workspace(PrefillArgs& a, void* ws, size_t bytes) {
+  a.num_cus = 0;
+  a.ws_slots = 0;
+  a.ws_o = nullptr;
+  a.ws_ml = nullptr;
+  a.ws_list = nullptr;
+  if (ws == nullptr || bytes < prefill_workspace_bytes()) return;   // no splitting
+  const size_t rows = 2 * (size_t)kMaxPrefillCus * kRows;
+  a.ws_o = static_cast<float*>(ws);
+  a.ws_ml = a.ws_o + rows * kHeadDim;
+  a.ws_list = reinterpret_cast<int32_t*>(a.ws_ml + rows * 2);
+  a.ws_slots = 2 * kMaxPrefillCus;
+}
+
+hipError_t launch_prefill_mfma(PrefillArgs a, int group, int num_tiles_total, hipStream_t stream) {
   if (num_tiles_total <= 0) return hipSuccess;
   switch (group) {
-    case 1: hipLaunchKernelGGL(prefill_mfma_kernel<1>, dim3(num_tiles_total), dim3(kThreads), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL(prefill_mfma_kernel<2>, dim3(num_tiles_total), dim3(kThreads), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL(prefill_mfma_kernel<4>, dim3(num_tiles_total), dim3(kThreads), 0, stream, a); break;
-    case 8: hipLaunchKernelGGL(prefill_mfma_kernel<8>, dim3(num_tiles_total), dim3(kThreads), 0, stream, a); break;
+    case 1: return launch_group<1>(a, num_tiles_total, stream);
+    case 2: return launch_group<2>(a, num_tiles_total, stream);
+    case 4: return launch_group<4>(a, num_tiles_total, stream);
+    case 8: return launch_group<8>(a, num_tiles_total, stream);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace bros

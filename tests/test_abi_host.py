@@ -174,7 +174,10 @@ def test_workspace_query():
     assert 0 < small < big and big % 16 == 0
     assert q(0, 1, 64, 32, 128, 16384) == big       # bf16 size does not grow with the context
     assert q(0, 1, 65, 32, 128, 8192) > big
-    assert q(1, 1, 2048, 32, 128, 8192) == 0        # bf16 prefill runs on the matrix cores, no scratch
+    # bf16 prefill on the matrix cores: the optional split workspace, one size for every call
+    split = q(1, 1, 2048, 32, 128, 8192)
+    assert split > 0 and split % 16 == 0 and split == q(1, 1, 16, 8, 128, 32768)
+    assert q(1, 1, 2048, 32, 128, 32769) != split   # beyond 32768: the vector path's own size
     assert q(1, 0, 2048, 32, 128, 8192) > 0
     assert q(0, 1, 4, 8, 64, 64) == 0               # unsupported head_dim
 

@@ -2,8 +2,10 @@
 
 The pools are written by the oracle's kv_write first (so the chunk's own K/V
 are in place) and then uploaded, so these tests exercise the prefill kernel
-alone. Covers the mixed-step workload's four 512-row chunks, c0 = 0 (pure
-causal), chunk starts and lengths off the 16/64 grid, one-row chunks, RT
+alone. Covers the mixed-step workload's four 512-row chunks (with the
+workspace and without), a long-context chunk whose units are split over their
+keys when they leave compute units idle, more units than the device-side plan
+holds, c0 = 0 (pure causal), chunk starts and lengths off the 16/64 grid, one-row chunks, RT
 chunks walking from the right, all group sizes, the fp32 path, NaN-poisoned
 unowned slots, and the last row against a decode at the same length."""
 
@@ -25,7 +27,7 @@ def written(batch):
     return batch
 
 
-def run_prefill(batch):
+def run_prefill(batch, workspace=True):
     torch = require_gpu()
     from paper_2504_09590_amd import bros
     dev = bros.to_device(batch)
@@ -35,7 +37,7 @@ def run_prefill(batch):
     max_q = int(np.diff(batch.cu_q).max())
     code = bros.BROS_F32 if batch.dtype == "f32" else bros.BROS_BF16
     wsb = bros.bros_attn_workspace_size(1, code, int(batch.cu_q[-1]), batch.num_q_heads, batch.head_dim, max_ctx)
-    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda") if wsb else None
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda") if wsb and workspace else None
     bros.bros_attn_prefill_chunk(out, dev.q_prefill, dev.cu_q, max_q, dev.k_pool, dev.v_pool,
                                  dev.block_tables[:P], dev.dir[:P], dev.cls[:P], dev.ctx_lens[:P], max_ctx,
                                  workspace=ws)
@@ -60,11 +62,37 @@ def chunk_batch(c0s, ns, classes, group=4, hkv=8, dtype="bf16", seed=0, dirs=Non
                     spare_blocks=5, dirs=dirs)
 
 
-def test_mixed_step_workload_prefill_chunks():
+@pytest.mark.parametrize("workspace", [True, False], ids=["workspace", "no-workspace"])
+def test_mixed_step_workload_prefill_chunks(workspace):
     b = written(W.generate(3))
-    announce(f"prefill llama3-8b-mixed-step chunks c0={(b.ctx_lens[:4] - 512).tolist()}")
-    mx, mean = compare(run_prefill(b), ref_prefill(b), "bf16", "mixed-step prefill")
+    announce(f"prefill llama3-8b-mixed-step chunks c0={(b.ctx_lens[:4] - 512).tolist()} workspace={workspace}")
+    mx, mean = compare(run_prefill(b, workspace), ref_prefill(b), "bf16", "mixed-step prefill")
     print(f"prefill max {mx:.3g} mean {mean:.3g}")
+
+
+@pytest.mark.parametrize("group,hkv", [(4, 2), (1, 8)])
+def test_long_context_chunk_split_into_pieces(group, hkv):
+    # fewer (row tile, KV head) units than compute units, one of them over ~390
+    # key tiles: with the workspace the long units are cut into pieces over
+    # their keys and merged. Both forms match the oracle; they differ from each
+    # other by rounding, which shows the split path ran.
+    b = written(chunk_batch([12000, 0, 7], [512, 64, 1], [W.RT] * 3, group=group, hkv=hkv, seed=34 + group))
+    poison_unowned(b)
+    announce(f"prefill c0=12000 n=512 beside short chunks G={group} Hkv={hkv} (split pieces)")
+    split, whole = run_prefill(b), run_prefill(b, workspace=False)
+    ref = ref_prefill(b)
+    compare(split, ref, "bf16", "long-context split")
+    compare(whole, ref, "bf16", "long-context whole units")
+    assert not np.array_equal(split, whole)
+
+
+def test_more_units_than_the_device_plan_holds():
+    # 17 chunks of 512 rows at G=4: 272 units per KV head, past the 256 the
+    # kernels plan on the device; every unit runs whole
+    c0 = [int(x) for x in np.random.default_rng(35).integers(0, 300, 17)]
+    b = written(chunk_batch(c0, [512] * 17, [W.RT] * 17, group=4, hkv=2, seed=35))
+    announce("prefill 17 x 512-row chunks (unit fallback)")
+    compare(run_prefill(b), ref_prefill(b), "bf16", "272 units")
 
 
 @pytest.mark.parametrize("group", [1, 2, 4, 8])
