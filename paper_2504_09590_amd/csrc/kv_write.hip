@@ -7,8 +7,8 @@
 // One workgroup moves kTokens tokens. Its 256 threads first request the
 // tokens' source rows (16-byte chunks), which do not depend on the
 // destination; meanwhile each thread checks one sequence's range of new
-// tokens and resolves the destination (position, table entry, slot) of
-// those that fall in this workgroup; then the chunks are stored. Writes are
+// tokens, and then one thread per token resolves its destination (position,
+// table entry, slot); then the chunks are stored. Writes are
 // slot-granular, so two sequences sharing a block never race.
 #include "bros_device.h"
 #include "bros_kernels.h"
@@ -24,6 +24,8 @@ typedef unsigned v4u_t __attribute__((ext_vector_type(4)));   // 16 bytes (a pla
 
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
+  __shared__ int s_seq[kTokens];   // the sequence holding each token, or -1
+  __shared__ int s_pos[kTokens];   // the token's position in it
   __shared__ int s_dst[kTokens];   // block * 16 + slot, or -1 when the token is skipped
 
   const int tid = threadIdx.x;
@@ -59,26 +61,33 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
     }
   }
 
-  // Destinations: thread j checks whether sequence j holds any of this
-  // workgroup's tokens (one round of loads: its prefix offsets, first position
-  // and direction), and resolves those tokens' table entries (a second round).
-  // A token in no sequence's range is skipped.
-  if (tid < kTokens) s_dst[tid] = -1;
+  // Destinations, in two rounds of loads. First, thread j checks whether
+  // sequence j holds any of this workgroup's tokens (its prefix offsets and
+  // first position) and notes, per token it holds, the sequence and position.
+  // Then thread t < kTokens resolves token t's table entry and direction, so
+  // that the tokens' lookups run side by side. A token in no sequence's
+  // range is skipped.
+  if (tid < kTokens) s_seq[tid] = -1;
   __syncthreads();
   for (int j = tid; j < a.num_seqs; j += kThreads) {
     const int lo = a.cu_new[j], hi = a.cu_new[j + 1];
     const int p0 = a.pos0[j];
     const int k0 = max(lo, t0), k1 = min(hi, min(t0 + kTokens, a.num_new_tokens));
     for (int k = k0; k < k1; ++k) {
-      const int p = p0 + (k - lo);
-      int dst = -1;
-      if (p >= 0 && (p >> 4) < a.max_blocks_per_seq) {
-        const int blk = a.block_tables[(size_t)j * a.max_blocks_per_seq + (p >> 4)];
-        const int dirv = entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, j, p >> 4);
-        if (blk >= 0 && blk < a.num_blocks) dst = blk * kBlockSize + slot_of_offset(p & 15, dirv);
-      }
-      s_dst[k - t0] = dst;
+      s_seq[k - t0] = j;
+      s_pos[k - t0] = p0 + (k - lo);
     }
+  }
+  __syncthreads();
+  if (tid < kTokens) {
+    const int j = s_seq[tid], p = s_pos[tid];
+    int dst = -1;
+    if (j >= 0 && p >= 0 && (p >> 4) < a.max_blocks_per_seq) {
+      const int blk = a.block_tables[(size_t)j * a.max_blocks_per_seq + (p >> 4)];
+      const int dirv = entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, j, p >> 4);
+      if (blk >= 0 && blk < a.num_blocks) dst = blk * kBlockSize + slot_of_offset(p & 15, dirv);
+    }
+    s_dst[tid] = dst;
   }
   __syncthreads();
 
