@@ -45,10 +45,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 4996952.0, 16491.3),
-    "llama3-8b-decode": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 455811.9, 5174.1),
-    "llama3-8b-mixed-step": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 1131361.9, 6151.3),
-    "llama3-8b-pressure": ("9ecc367610185c42a27f59ef39a7292af2ca45adb3cb18e605b5c5a7e5a6dd23", 609531.9, 10093.4),
+    "llama3-70b-decode": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 4996737.2, 16490.8),
+    "llama3-8b-decode": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 455807.1, 5173.8),
+    "llama3-8b-mixed-step": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 1131342.1, 6150.2),
+    "llama3-8b-pressure": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 609521.9, 10093.3),
 }
 
 
