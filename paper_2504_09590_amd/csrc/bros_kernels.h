@@ -85,6 +85,7 @@ struct PrefillArgs {
   // the list of split units that the merge walks (count, then (item, parts,
   // first slot) triples).
   int32_t num_cus;
+  int32_t xcd_cus;        // compute units per XCD when the launch has the whole chip, else 0
   int32_t ws_slots;
   float* ws_o;
   float* ws_ml;

@@ -30,7 +30,8 @@
 // Data path. K and V rows go straight from the pool into LDS
 // (global_load_lds, no registers), row-major [key][d] with the 16-byte chunks
 // of row r permuted by chunk ^ swz(r), which makes both the K operand reads
-// and the transposing V^T reads (ds_read_b64_tr_b16) free of bank conflicts.
+// and the transposing V^T reads (ds_read_b64_tr_b16) free of bank conflicts
+// (64 banks of 4 bytes).
 // K and V have rings of their own (four slots each): the K tile of step i + 1
 // is read while the V tile of step i is, and each slot is refilled four steps
 // ahead of its use. The unit's table entries are validated once into LDS and
@@ -82,6 +83,7 @@ constexpr int kMaxRankItems = kThreads;            // units planned on the devic
 constexpr int kMaxPieces = 2 * kThreads;           // pieces ranked on the device (two per thread)
 constexpr int kMinPartTiles = 8;                   // the shortest piece a unit is split into
 constexpr int kLoadsPerStep = 4;                   // two K and two V loads per wave per step
+constexpr int kXcds = 8;                           // accelerator dies of the chip; blockIdx % 8 picks the die
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(v4u_t v) { return __builtin_bit_cast(bf16x8_t, v); }
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {   // round to nearest even
@@ -89,7 +91,11 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {   // round 
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 // 16-byte chunk c of row r of a K or V tile sits at byte r * 256 + 16 * (c ^ swz(r)).
-__device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+// The row's four bits are permuted (r1 r0 r2 r3): the 16 rows a K read
+// serves in one pass see 16 different chunks, and the four keys a transposing
+// V read serves in one pass (rows 4h .. 4h + 3, plus 8) see four different
+// 64-byte groups, so neither read meets a bank conflict with 64 banks.
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | (((r >> 2) & 1) << 1) | ((r >> 3) & 1); }
 
 __device__ __forceinline__ uint2 lds_read_tr(const uint8_t* p) {   // ds_read_b64_tr_b16
   const v4s_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -337,11 +343,22 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a
   // ---- Which piece: rank by key tiles, longest first (ties by index). Ids
   // r * Hkv + g give every rank all KV heads on consecutive ids, i.e. on
   // different XCDs (id % 8), and one KV head of every unit on one XCD when
-  // Hkv is a multiple of 8.
+  // Hkv is a multiple of 8. Workgroup j of an XCD (blockIdx = 8 j + x) first
+  // lands on compute unit j of the XCD, and workgroup j + C (C compute units
+  // per XCD) on the same unit's second slot; the second slots take the
+  // remaining ranks in reverse, so the longest unit of a compute unit shares
+  // it with the shortest and every unit's pair carries about the same work.
   const int Hkv = a.num_kv_heads;
   const int tps = a.tiles_per_seq;
-  const int g = blockIdx.x % Hkv;
-  const int rank = blockIdx.x / Hkv;
+  int id = blockIdx.x;
+  if (a.xcd_cus > 0) {
+    const int x = id % kXcds, j = id / kXcds;
+    const int C = a.xcd_cus;
+    const int R = min(((int)gridDim.x - x + kXcds - 1) / kXcds, 2 * C);   // this XCD's first-round workgroups
+    if (j >= C && j < R) id = (R - 1 - (j - C)) * kXcds + x;
+  }
+  const int g = id % Hkv;
+  const int rank = id / Hkv;
   // (the K ring is free until the first loads)
   const PiecePlan plan = plan_pieces<QT>(a, rank, reinterpret_cast<int*>(s_kring));
   const int item = __builtin_amdgcn_readfirstlane(plan.item);
@@ -844,6 +861,13 @@ hipError_t launch_group(PrefillArgs a, int num_units, hipStream_t stream) {
     int cus = stream_compute_units(stream);
     cus = cus < kMaxPrefillCus ? cus : kMaxPrefillCus;
     if (num_units < cus) a.num_cus = cus;
+  }
+  // Placement of the first round (two workgroups per compute unit): known
+  // when the stream has the whole chip, so unsplit units are paired by work.
+  a.xcd_cus = 0;
+  if (a.num_cus == 0) {
+    const int cus = stream_compute_units(stream);
+    if (cus == stream_compute_units(nullptr) && cus % kXcds == 0) a.xcd_cus = cus / kXcds;
   }
   // ranks beyond the units: at most num_cus / Hkv more pieces than items
   const long long grid = (long long)num_units + a.num_cus;
