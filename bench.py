@@ -45,10 +45,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 4996737.2, 16490.8),
-    "llama3-8b-decode": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 455807.1, 5173.8),
-    "llama3-8b-mixed-step": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 1131342.1, 6150.2),
-    "llama3-8b-pressure": ("3e2356ea82528f4a1dbbdf4547a00b495e0884116f57d69e4a870c5809a5d113", 609521.9, 10093.3),
+    "llama3-70b-decode": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 4996842.9, 16491.8),
+    "llama3-8b-decode": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 455818.3, 5174.0),
+    "llama3-8b-mixed-step": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 1131377.4, 6150.6),
+    "llama3-8b-pressure": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 609542.5, 10092.8),
 }
 
 
