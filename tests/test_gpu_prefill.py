@@ -27,7 +27,7 @@ def written(batch):
     return batch
 
 
-def run_prefill(batch, workspace=True):
+def run_prefill(batch, workspace=True, ws_bytes=None):
     torch = require_gpu()
     from paper_2504_09590_amd import bros
     dev = bros.to_device(batch)
@@ -37,6 +37,8 @@ def run_prefill(batch, workspace=True):
     max_q = int(np.diff(batch.cu_q).max())
     code = bros.BROS_F32 if batch.dtype == "f32" else bros.BROS_BF16
     wsb = bros.bros_attn_workspace_size(1, code, int(batch.cu_q[-1]), batch.num_q_heads, batch.head_dim, max_ctx)
+    if ws_bytes is not None:
+        wsb = ws_bytes
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda") if wsb and workspace else None
     bros.bros_attn_prefill_chunk(out, dev.q_prefill, dev.cu_q, max_q, dev.k_pool, dev.v_pool,
                                  dev.block_tables[:P], dev.dir[:P], dev.cls[:P], dev.ctx_lens[:P], max_ctx,
@@ -84,6 +86,8 @@ def test_long_context_chunk_split_into_pieces(group, hkv):
     compare(split, ref, "bf16", "long-context split")
     compare(whole, ref, "bf16", "long-context whole units")
     assert not np.array_equal(split, whole)
+    # a workspace smaller than the query is accepted and splits nothing
+    assert np.array_equal(run_prefill(b, ws_bytes=4096), whole)
 
 
 def test_more_units_than_the_device_plan_holds():
