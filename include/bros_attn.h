@@ -203,7 +203,9 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
  * Bytes of device workspace the call `kind` needs for `num_rows` query rows
  * (num_seqs for decode, num_q_tokens for prefill). Pure host arithmetic; it
  * does not know num_kv_heads and sizes bf16 decode for groups of up to 8
- * query heads. Returns 0 for unsupported arguments.
+ * query heads. For the bf16 prefill on the matrix cores (max_ctx <= 32768)
+ * it returns the size of the optional split workspace, the same for every
+ * call. Returns 0 for unsupported arguments.
  */
 size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
                                 int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);
