@@ -49,3 +49,39 @@ def test_mixed_step_full(mixed, overlap, prefill_cus, swap_slots, copy_cus):
     mx_p, mean_p = compare(bros.to_host_bits(pre), pre_ref, "bf16", "step prefill")
     mx_d, mean_d = compare(bros.to_host_bits(dec), dec_ref, "bf16", "step decode")
     print(f"step prefill max {mx_p:.3g} mean {mean_p:.3g}; decode max {mx_d:.3g} mean {mean_d:.3g}")
+
+
+def test_mixed_step_replays_from_a_hip_graph(mixed):
+    """The whole step (write, prefill, decode) captured once in a HIP graph and
+    replayed: every replay, with eager work and synchronisations between them,
+    gives the eager step's outputs bit for bit (the kernels allocate nothing
+    and clear nothing with memset, so a serving loop can capture them)."""
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    from paper_2504_09590_amd.step import MixedStep
+    b, (k1, v1, pre_ref, dec_ref) = mixed
+    dev = bros.to_device(b)
+    announce(f"mixed step {b.name} captured in a HIP graph")
+    step = MixedStep(b, dev)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        pre, dec = step.run()       # eager, also warms the library's per-device queries
+        side.synchronize()
+        eager = (bros.to_host_bits(pre).copy(), bros.to_host_bits(dec).copy())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            step.run()
+    for i in range(3):
+        scratch = torch.randn(1 << 20, device="cuda")     # eager work between the replays
+        pre.fill_(float("nan"))
+        dec.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert float(scratch.abs().sum()) > 0
+        assert np.array_equal(bros.to_host_bits(pre), eager[0]), f"prefill, replay {i}"
+        assert np.array_equal(bros.to_host_bits(dec), eager[1]), f"decode, replay {i}"
+    step.close()
+    compare(eager[0], pre_ref, "bf16", "step prefill (eager)")
+    compare(eager[1], dec_ref, "bf16", "step decode (eager)")
+    for name, ref, got in (("k", k1, dev.k_pool), ("v", v1, dev.v_pool)):
+        assert np.array_equal(bros.to_host_bits(got), ref), f"{name} pool after the replays"
