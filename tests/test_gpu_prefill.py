@@ -4,7 +4,9 @@ The pools are written by the oracle's kv_write first (so the chunk's own K/V
 are in place) and then uploaded, so these tests exercise the prefill kernel
 alone. Covers the mixed-step workload's four 512-row chunks (with the
 workspace and without), a long-context chunk whose units are split over their
-keys when they leave compute units idle, more units than the device-side plan
+keys when they leave compute units idle, an empty chunk between others, the
+longest context of the matrix-core path (its whole table in LDS; split into
+128 pieces per unit with the workspace), more units than the device-side plan
 holds, c0 = 0 (pure causal), chunk starts and lengths off the 16/64 grid, one-row chunks, RT
 chunks walking from the right, all group sizes, the fp32 path, NaN-poisoned
 unowned slots, and the last row against a decode at the same length."""
@@ -88,6 +90,25 @@ def test_long_context_chunk_split_into_pieces(group, hkv):
     assert not np.array_equal(split, whole)
     # a workspace smaller than the query is accepted and splits nothing
     assert np.array_equal(run_prefill(b, ws_bytes=4096), whole)
+
+
+def test_empty_chunk_between_others():
+    # a sequence with no new rows in the length table is skipped; its neighbours are not
+    b = written(chunk_batch([10, 50, 0], [40, 0, 65], [W.RT] * 3, group=4, hkv=2, seed=36))
+    poison_unowned(b)
+    announce("prefill with an empty chunk between two others")
+    compare(run_prefill(b), ref_prefill(b), "bf16", "empty chunk")
+
+
+@pytest.mark.parametrize("workspace", [False, True], ids=["whole", "split"])
+def test_longest_context_of_the_matrix_core_path(workspace):
+    # ctx = 32768 exactly: the whole 2048-entry table staged in LDS; with the
+    # workspace the two units (one KV head) are cut into 128 pieces each
+    b = written(chunk_batch([32768 - 40], [40], [W.RT], group=4, hkv=1, seed=37))
+    assert int(b.ctx_lens[0]) == 32768
+    poison_unowned(b)
+    announce(f"prefill ctx 32768 (the matrix-core path's limit), workspace={workspace}")
+    compare(run_prefill(b, workspace), ref_prefill(b), "bf16", f"ctx 32768 {'split' if workspace else 'whole'}")
 
 
 def test_more_units_than_the_device_plan_holds():
