@@ -190,7 +190,6 @@ def main():
                          "overlapping the attention")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--check", action="store_true", help="check the benchmarked step against the oracle first")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy K times (scales FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
@@ -227,17 +226,6 @@ def main():
                      copy_cus=args.copy_cus, swap_serial=args.swap_serial)
     work = algorithmic_work(batch)
     stream = step.main if step.main is not None else torch.cuda.current_stream()
-
-    if args.check:
-        sys.path.insert(0, os.path.join(ROOT, "tests"))
-        from tests.gpu_helpers import compare, oracle_step
-        k1, v1, pre_ref, dec_ref = oracle_step(batch)
-        pre, dec = step.run()
-        torch.cuda.synchronize()
-        if batch.num_prefill:
-            compare(bros.to_host_bits(pre), pre_ref, batch.dtype, "prefill")
-        compare(bros.to_host_bits(dec), dec_ref, batch.dtype, "decode")
-        print("check: step matches the oracle", file=sys.stderr)
 
     for _ in range(args.warmup):
         step.run()
