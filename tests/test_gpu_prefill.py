@@ -29,7 +29,7 @@ def written(batch):
     return batch
 
 
-def run_prefill(batch, workspace=True, ws_bytes=None):
+def run_prefill(batch, workspace=True, ws_bytes=None, stream=None):
     torch = require_gpu()
     from paper_2504_09590_amd import bros
     dev = bros.to_device(batch)
@@ -44,7 +44,7 @@ def run_prefill(batch, workspace=True, ws_bytes=None):
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda") if wsb and workspace else None
     bros.bros_attn_prefill_chunk(out, dev.q_prefill, dev.cu_q, max_q, dev.k_pool, dev.v_pool,
                                  dev.block_tables[:P], dev.dir[:P], dev.cls[:P], dev.ctx_lens[:P], max_ctx,
-                                 workspace=ws)
+                                 workspace=ws, stream=stream)
     torch.cuda.synchronize()
     return bros.to_host_bits(out)
 
@@ -90,6 +90,23 @@ def test_long_context_chunk_split_into_pieces(group, hkv):
     assert not np.array_equal(split, whole)
     # a workspace smaller than the query is accepted and splits nothing
     assert np.array_equal(run_prefill(b, ws_bytes=4096), whole)
+
+
+def test_split_on_a_compute_unit_share():
+    # the split sizes its pieces by the stream's compute units: 96 units on a
+    # 128-CU share are still split (and 128 more ranks launched)
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    b = written(chunk_batch([12000, 0, 7], [512, 64, 1], [W.RT] * 3, group=4, hkv=2, seed=38))
+    poison_unowned(b)
+    announce("prefill split on a 128-CU stream")
+    share = bros.bros_stream_create_cu_share(0, 128)
+    try:
+        got = run_prefill(b, stream=share)
+    finally:
+        torch.cuda.synchronize()
+        bros.bros_stream_destroy(share)
+    compare(got, ref_prefill(b), "bf16", "split on a CU share")
 
 
 def test_empty_chunk_between_others():
