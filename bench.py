@@ -9,12 +9,17 @@ new tokens on c0 ~ U{0..2048} cached tokens, 128 BE decode rows with ctx ~
 U{512..8192}, 32 q / 8 KV heads, head_dim 128, bf16, 40000-block pool).
 
 Timing: inputs resident in HBM; W untimed warm-up steps, then exactly K steps
-between two synchronizations, with HIP events around each of the three calls
-on the stream they run on. Prints ONE JSON line:
+between two synchronizations, with HIP events around the decode call on the
+stream it runs on (a second pass of K steps brackets every call, for the
+per-call figures). Then R single steps, each after a scrub that reads and
+writes 1 GiB outside its events, give the median, p10 and p90 of a step whose
+KV comes from HBM. Prints ONE JSON line:
   value     = algorithmic bytes of a step / step time (GB/s, whole job)
   roofline  = the dominant call (decode): algorithmic bytes per launch / its
               average event-timed duration, against 8 TB/s HBM
-  cpu_baseline = the CPU oracle on a bounded sample of the same workload.
+  scrubbed  = p10 / p50 / p90 of the scrubbed single steps
+  cpu_baseline = the CPU oracle timed on one host core over one whole step
+              (or, when the pools do not fit in float64, a sample of rows).
 """
 
 from __future__ import annotations
@@ -33,6 +38,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
 METRIC = "µs per mixed RT/BE attention step + achieved KV GB/s (% of HBM peak)"
+# The oracle runs one whole step when both pools widened to float64 fit in this many bytes.
+FP64_POOL_LIMIT = 16e9
+# Bytes the scrub between timed repetitions reads and writes (4x the 256 MiB last-level cache).
+SCRUB_BYTES = 1 << 30
 
 # HBM traffic of the decode call from rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, one
 # counter per run, KiB per dispatch, summed over decode_mfma_kernel and decode_mfma_merge_kernel).
@@ -98,39 +107,55 @@ def algorithmic_work(batch):
     }
 
 
-def cpu_baseline(batch, budget_s: float):
-    """Time the oracle (as it stands) on a bounded sample of this workload:
-    decode rows in batch order until the budget is used, plus the whole first
-    prefill chunk. Returns GB/s of algorithmic bytes processed."""
+def cpu_baseline(batch, budget_s: float, step_bytes: int):
+    """The oracle, as it stands, timed on one host core (BLAS limited to one
+    thread). When the pools fit in float64 within FP64_POOL_LIMIT, it runs one
+    whole step of the workload: kv_write, prefill_chunk over every chunk and
+    decode over every row, one oracle call each on the same inputs (each call
+    widens the whole pool once). Otherwise it runs decode rows in batch order,
+    each on a pool cut to that row's blocks, until `budget_s` is spent, and the
+    rate is scaled to the step. Returns GB/s of algorithmic bytes and seconds
+    per step."""
     import oracle
-    t0 = time.perf_counter()
+    from threadpoolctl import threadpool_limits
+
+    from paper_2504_09590_amd import workload
     P = batch.num_prefill
-    e = batch.elem_bytes
-    kv_tok = 2 * batch.num_kv_heads * batch.head_dim * e
-    done_bytes = 0
-    desc = []
-    if P:
-        oracle.prefill_chunk(batch.q_prefill, batch.cu_q, batch.k_pool, batch.v_pool, batch.block_tables[:P],
-                             batch.dir[:P], batch.ctx_lens[:P], batch.dtype, seqs=[0])
-        done_bytes += int(batch.ctx_lens[0]) * kv_tok
-        desc.append(f"prefill chunk 0 ({int(batch.cu_q[1])} rows, ctx {int(batch.ctx_lens[0])})")
-    rows = 0
-    for s in range(batch.num_seqs - P):
-        if time.perf_counter() - t0 > budget_s:
-            break
-        oracle.decode(batch.q_decode, batch.k_pool, batch.v_pool, batch.block_tables[P:], batch.dir[P:],
-                      batch.ctx_lens[P:], batch.dtype, seqs=[s])
-        done_bytes += int(batch.ctx_lens[P + s]) * kv_tok
-        rows += 1
-    dt = time.perf_counter() - t0
-    desc.append(f"{rows} of {batch.num_seqs - P} decode rows")
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([1] + [int(p.get("num_threads", 1)) for p in threadpool_info()])
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
-    return {"value": done_bytes / dt / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
-            "sample": "; ".join(desc) + f"; {dt:.1f} s fp64 NumPy", "seconds": round(dt, 2)}
+    kv_tok = 2 * batch.num_kv_heads * batch.head_dim * batch.elem_bytes
+    whole = 2 * batch.k_pool.size * 8 <= FP64_POOL_LIMIT
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        if whole:
+            k1, v1 = oracle.kv_write(batch.k_pool, batch.v_pool, batch.k_new, batch.v_new, batch.block_tables,
+                                     batch.dir, batch.pos0, batch.cu_new)
+            if P:
+                oracle.prefill_chunk(batch.q_prefill, batch.cu_q, k1, v1, batch.block_tables[:P], batch.dir[:P],
+                                     batch.ctx_lens[:P], batch.dtype)
+            if batch.num_seqs > P:
+                oracle.decode(batch.q_decode, k1, v1, batch.block_tables[P:], batch.dir[P:], batch.ctx_lens[P:],
+                              batch.dtype)
+            dt = time.perf_counter() - t0
+            per_step = dt
+            sample = (f"whole step: kv_write of {int(batch.cu_new[-1])} tokens, {P} prefill chunks, "
+                      f"{batch.num_seqs - P} decode rows; {dt:.1f} s fp64 NumPy on one core")
+        else:
+            done, rows = 0, 0
+            for r in range(batch.num_seqs - P):
+                if time.perf_counter() - t0 > budget_s:
+                    break
+                s = P + r
+                tab, kp, vp = workload.compact_pool(batch.block_tables[s:s + 1], batch.ctx_lens[s:s + 1],
+                                                    batch.k_pool, batch.v_pool)
+                oracle.decode(batch.q_decode[r:r + 1], kp, vp, tab, batch.dir[s:s + 1], batch.ctx_lens[s:s + 1],
+                              batch.dtype)
+                done += int(batch.ctx_lens[s]) * kv_tok
+                rows += 1
+            dt = time.perf_counter() - t0
+            per_step = dt * step_bytes / max(done, 1)
+            sample = (f"{rows} of {batch.num_seqs - P} decode rows in batch order, each on a pool cut to its "
+                      f"blocks; {dt:.1f} s fp64 NumPy on one core, scaled to the step")
+    return {"value": round(step_bytes / per_step / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": sample, "seconds_per_step": round(per_step, 2), "seconds": round(dt, 2)}
 
 
 def swap_figures(step, per_call, K):
@@ -188,7 +213,10 @@ def main():
     ap.add_argument("--swap-slots", type=int, default=0,
                     help="also checkpoint and restore N slots per step (lazy checkpointing), the host copies "
                          "overlapping the attention")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--reps", type=int, default=50,
+                    help="single steps timed one by one after a cache scrub each (median, p10, p90)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for cpu_baseline when the whole step does not fit in memory")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy K times (scales FETCH_SIZE / WRITE_SIZE counters)")
@@ -282,10 +310,45 @@ def main():
         per = {k: float(np.mean([a.elapsed_time(b) for a, b in pairs])) for k, pairs in ev.items()}
         return start.elapsed_time(end) / K, per, wall
 
-    # the headline pass (decode events only), then a pass with every call bracketed
+    def scrubbed_reps(R: int):
+        """R single steps, each preceded (outside its events) by a scrub that
+        reads and writes SCRUB_BYTES, so that no KV of the previous step is
+        left in the last-level cache. Returns the step times in ms."""
+        scrub = torch.zeros(SCRUB_BYTES // 4, dtype=torch.float32, device=dev.k_pool.device)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(R)]
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            for a, b in ev:
+                scrub.add_(1.0)
+                a.record(stream)
+                if step.swap:
+                    step.swap_out(stream)
+                step.kv_write(stream)
+                if step.swap:
+                    step.swap_in(stream)
+                if step.overlap:
+                    a2 = torch.cuda.Event()
+                    a2.record(stream)
+                    side.wait_event(a2)
+                step.prefill(side)
+                step.decode(stream)
+                if step.overlap:
+                    b2 = torch.cuda.Event()
+                    b2.record(side)
+                    stream.wait_event(b2)
+                if step.swap:
+                    step.swap_next(stream)
+                b.record(stream)
+        torch.cuda.synchronize()
+        del scrub
+        return np.array([a.elapsed_time(b) for a, b in ev])
+
+    # the headline pass (decode events only), then a pass with every call
+    # bracketed, then single steps with a cache scrub before each
     ms, per_head, wall_ms = timed_steps(False)
     ms_inst, per_call, _ = timed_steps(True)
     per_call["decode_in_headline_pass"] = per_head["decode"]
+    reps = scrubbed_reps(max(args.reps, 1))
 
     dec_ms = per_head.get("decode")
     roof = None
@@ -311,6 +374,10 @@ def main():
                    "swap_serial": bool(args.swap_serial)},
         "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
         "us_per_step_every_call_timed": round(ms_inst * 1e3, 2),
+        "scrubbed": {"scrub": True, "scrub_bytes": SCRUB_BYTES, "reps": int(reps.size),
+                     "us_p10": round(float(np.percentile(reps, 10)) * 1e3, 2),
+                     "us_p50": round(float(np.percentile(reps, 50)) * 1e3, 2),
+                     "us_p90": round(float(np.percentile(reps, 90)) * 1e3, 2)},
         "step_bytes": work["step_bytes"],
         "roofline": roof,
         "wall_ms_timed_region": round(wall_ms, 3),
@@ -323,7 +390,7 @@ def main():
         line["swap"] = swap_figures(step, per_call, K)
     step.close()
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget)
+        line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget, work["step_bytes"])
     print(json.dumps(line), flush=True)
 
 

@@ -406,3 +406,28 @@ def custom(ctx, cls, num_q_heads, num_kv_heads, head_dim=128, dtype="bf16", seed
         v_pool=pool_values(seed, 6, int(num_blocks), hkv, d, dtype),
         seed=seed, meta={"shared_tail_pairs": len(pairs)},
     )
+
+
+# ---------------------------------------------------------------------------
+# a pool holding only the blocks some sequences reference
+# ---------------------------------------------------------------------------
+
+def compact_pool(block_tables, ctx_lens, k_pool, v_pool):
+    """The pool blocks that entries [0, ceil(ctx / 16)) of these table rows
+    reference, renumbered 0 .. n-1 in id order, and the rows rewritten to the
+    new ids (-1 in every other entry). A sequence's cache is the same through
+    the new rows and the smaller pool, so a consumer that reads only the blocks
+    a table references sees the same values with far less memory. Entries
+    outside [0, num_blocks) stay -1."""
+    tables = np.asarray(block_tables)
+    ctx = np.asarray(ctx_lens, dtype=np.int64)
+    nblk = _block_counts(np.maximum(ctx, 0))
+    used = np.arange(tables.shape[1])[None, :] < nblk[:, None]
+    ids = tables[used]
+    ids = np.unique(ids[(ids >= 0) & (ids < k_pool.shape[0])])
+    remap = np.full(k_pool.shape[0], -1, dtype=np.int64)
+    remap[ids] = np.arange(len(ids))
+    ok = used & (tables >= 0) & (tables < k_pool.shape[0])
+    out = np.full(tables.shape, -1, dtype=np.int32)
+    out[ok] = remap[tables[ok]]
+    return out, k_pool[ids], v_pool[ids]

@@ -134,3 +134,31 @@ def test_custom_batch_is_consistent():
     counts = oracle.slot_owner_counts(b.block_tables, b.dir, b.ctx_lens, b.num_blocks)
     assert counts.max() <= 1
     assert b.meta["shared_tail_pairs"] >= 1
+
+
+def test_compact_pool_keeps_every_sequence_cache():
+    # A pool cut down to the referenced blocks, through the rewritten tables,
+    # holds each sequence's cache unchanged (the oracle's own gather reads it).
+    b = W.custom([40, 17, 70, 9, 33], [W.RT, W.BE, W.BE, W.RT, W.RT], 8, 4, seed=21, spare_blocks=11)
+    rows = [1, 2, 4]
+    tab, kp, vp = W.compact_pool(b.block_tables[rows], b.ctx_lens[rows], b.k_pool, b.v_pool)
+    assert kp.shape[0] < b.num_blocks
+    for i, s in enumerate(rows):
+        ctx = int(b.ctx_lens[s])
+        full = oracle.gather_kv(b.k_pool, b.block_tables, b.dir, s, ctx)
+        small = oracle.gather_kv(kp, tab, b.dir[rows], i, ctx)
+        assert np.array_equal(full, small)
+        assert np.array_equal(oracle.gather_kv(b.v_pool, b.block_tables, b.dir, s, ctx),
+                              oracle.gather_kv(vp, tab, b.dir[rows], i, ctx))
+    nb = (b.ctx_lens[rows] + 15) // 16
+    assert np.all(tab[np.arange(tab.shape[1])[None, :] >= nb[:, None]] == -1)
+
+
+def test_oracle_rows_runner_matches_one_oracle_call():
+    # The child runner used by the full-size GPU tests gives the same float64
+    # rows as a single oracle call over the whole pool.
+    from tests.oracle_rows import decode_all_rows
+    b = W.custom([300, 17, 1000, 64, 5, 129], [W.BE, W.RT, W.BE, W.RT, W.BE, W.RT], 16, 4, seed=22,
+                 spare_blocks=5)
+    ref = oracle.decode(b.q_decode, b.k_pool, b.v_pool, b.block_tables, b.dir, b.ctx_lens, b.dtype)
+    assert np.array_equal(decode_all_rows(b, workers=2), ref)
