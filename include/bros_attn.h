@@ -211,6 +211,35 @@ size_t bros_attn_workspace_size(int32_t kind, int32_t dtype, int32_t num_rows,
                                 int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);
 
 /*
+ * bros_attn_decode_noalloc -- bros_attn_decode without a caller workspace.
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc. Same
+ * arguments, meaning and results as bros_attn_decode (the same kernels run),
+ * minus the workspace: the call uses a static device array of
+ * BROS_NOALLOC_SCRATCH_BYTES bytes that every GPU the library runs on holds
+ * until the process ends. It allocates and frees nothing. The caller still
+ * owns q, out, the pools and the metadata.
+ *
+ * Limit: a batch whose bros_attn_workspace_size(BROS_WS_DECODE, ...) exceeds
+ * BROS_NOALLOC_SCRATCH_BYTES is rejected with BROS_E_WORKSPACE before
+ * anything is launched (bf16: about num_seqs * num_q_heads * 520 bytes plus
+ * 17 MiB, so up to about 60 000 (row, query head) pairs).
+ * All calls on one GPU share that GPU's array and it keeps the last call's
+ * contents: calls that overlap in time on one GPU (two streams, two threads)
+ * race on it and must be serialised by the caller. The first call on a device
+ * resolves the array's address there (BROS_E_HIP if the runtime cannot).
+ */
+#define BROS_NOALLOC_SCRATCH_BYTES (48u << 20)
+int bros_attn_decode_noalloc(void* out, const void* q,
+                             const void* k_pool, const void* v_pool, int32_t num_blocks,
+                             const int32_t* block_tables, int32_t max_blocks_per_seq,
+                             const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry,
+                             const int32_t* ctx_lens, int32_t max_ctx, int32_t num_seqs,
+                             int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                             int32_t block_size, float scale, int32_t dtype, void* stream);
+
+/*
  * bros_kv_gather / bros_kv_scatter -- lazy checkpointing of shared blocks.
  *
  * Defines: Sec. 5.2 (lazy checkpointing): once a shared block has no empty

@@ -24,7 +24,7 @@ STATUS = {0: "BROS_OK", -1: "BROS_E_NULL", -2: "BROS_E_SHAPE", -3: "BROS_E_DTYPE
           -8: "BROS_E_NOMEM"}
 
 EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_write",
-            "bros_attn_decode", "bros_attn_prefill_chunk", "bros_attn_workspace_size",
+            "bros_attn_decode", "bros_attn_decode_noalloc", "bros_attn_prefill_chunk", "bros_attn_workspace_size",
             "bros_check_batch", "bros_stream_create_cu_share", "bros_stream_destroy",
             "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma",
             "bros_mgr_create", "bros_mgr_destroy", "bros_mgr_add_request", "bros_mgr_release", "bros_mgr_grow",
@@ -57,6 +57,8 @@ def _load() -> ctypes.CDLL:
     lib.bros_kv_write.restype = ctypes.c_int
     lib.bros_attn_decode.argtypes = [P, P, P, P, I, P, I, P, P, I, P, I, I, I, I, I, I, F, I, P, Z, P]
     lib.bros_attn_decode.restype = ctypes.c_int
+    lib.bros_attn_decode_noalloc.argtypes = [P, P, P, P, I, P, I, P, P, I, P, I, I, I, I, I, I, F, I, P]
+    lib.bros_attn_decode_noalloc.restype = ctypes.c_int
     lib.bros_attn_prefill_chunk.argtypes = [P, P, P, I, I, P, P, I, P, I, P, P, I, P, I, I, I, I, I, I, F, I, P, Z, P]
     lib.bros_attn_prefill_chunk.restype = ctypes.c_int
     lib.bros_attn_workspace_size.argtypes = [I, I, I, I, I, I]
@@ -154,6 +156,18 @@ def bros_attn_decode(out, q, k_pool, v_pool, block_tables, dir, cls, ctx_lens, m
                                 int(block_tables.shape[1]), _ptr(dir), _ptr(cls), _dir_mode(dir, block_tables),
                                 _ptr(ctx_lens), int(max_ctx), int(ctx_lens.shape[0]), int(q.shape[1]), hkv, d, bs,
                                 float(scale), _dtype_code(q), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def bros_attn_decode_noalloc(out, q, k_pool, v_pool, block_tables, dir, cls, ctx_lens, max_ctx: int,
+                             scale: float = 0.0, stream=None):
+    """bros_attn_decode with the library's static scratch array as its workspace
+    (for callers that cannot allocate); rejects batches beyond the array."""
+    nb, hkv, bs, d = (int(x) for x in k_pool.shape)
+    _check(LIB.bros_attn_decode_noalloc(_ptr(out), _ptr(q), _ptr(k_pool), _ptr(v_pool), nb, _ptr(block_tables),
+                                        int(block_tables.shape[1]), _ptr(dir), _ptr(cls),
+                                        _dir_mode(dir, block_tables), _ptr(ctx_lens), int(max_ctx),
+                                        int(ctx_lens.shape[0]), int(q.shape[1]), hkv, d, bs, float(scale),
+                                        _dtype_code(q), _stream(stream)))
 
 
 def bros_attn_prefill_chunk(out, q, cu_q, max_q_len: int, k_pool, v_pool, block_tables, dir, cls,

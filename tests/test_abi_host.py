@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings_and_version():
     for code, name in bros.STATUS.items():
         assert bros.LIB.bros_status_str(code).decode() == name
-    assert bros.LIB.bros_abi_version() == 6
+    assert bros.LIB.bros_abi_version() == 7
 
 
 # --- argument validation (returns before any HIP call) -----------------------
@@ -274,3 +274,19 @@ def test_checker_agrees_with_oracle_on_random_batches():
         except bros.BrosError:
             got_ok = False
         assert got_ok == expect_ok, (trial, tables, dirs, ctx)
+
+
+def test_noalloc_decode_rejects_a_batch_beyond_its_scratch_array():
+    # Checked before any HIP call: 4096 rows x 32 heads need more workspace
+    # than the static array holds (NULL tensors are never reached).
+    need = bros.bros_attn_workspace_size(bros.BROS_WS_DECODE, bros.BROS_BF16, 4096, 32, 128, 8192)
+    assert need > (48 << 20)
+    st = bros.LIB.bros_attn_decode_noalloc(None, None, None, None, 10, None, 4, None, None, 0, None, 8192, 4096,
+                                           32, 8, 128, 16, 0.0, bros.BROS_BF16, None)
+    assert st == -5
+    msg = bros.LIB.bros_last_error().decode()
+    assert "scratch" in msg and str(need) in msg
+    # within the limit the size check passes and the usual argument checks answer
+    st = bros.LIB.bros_attn_decode_noalloc(None, None, None, None, 10, None, 4, None, None, 0, None, 64, 2,
+                                           32, 8, 128, 16, 0.0, bros.BROS_BF16, None)
+    assert st == -1
