@@ -46,6 +46,7 @@ struct DecodeArgs {
   float* ws_acc;          // [slots][D] unnormalised partial outputs
   float* ws_ml;           // [slots][2] (running max in log2 units, sum)
   int32_t* ws_rows;       // bf16: first tile of each row, [rows + 1]
+  int32_t* ws_cut;        // bf16: per worker, the (row * Hkv + g) segment it starts and leaves cut, else -1
   int32_t num_workers;    // bf16: waves of the grid (workers beyond the tile count idle)
   int32_t num_rows;
   int32_t num_seqs;

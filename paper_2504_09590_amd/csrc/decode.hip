@@ -282,6 +282,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                                                      __builtin_bit_cast(bf16x8_t, qf[k]), sc, 0, 0, 0);
     }
     const bool seg_end = c0.b == c0.nblk - 1 || i + 1 == n;
+    if (i + 1 == n) {
+      // this worker's entry of the cut list: the segment it started and
+      // leaves unfinished (the merge folds it), else -1
+      const bool starts_cut = whole && c0.b != c0.nblk - 1;
+      if (lane == 0) a.ws_cut[wid] = starts_cut ? c0.row * nkv + c0.g : -1;
+    }
     // K and query registers are free: keys kDepth tiles ahead (and the query
     // of the next tile's segment)
     if (i + kDepth < n) issue_k(kf, blk[kDepth], cur[kDepth].g);
@@ -392,74 +398,99 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   }
 }
 
-// Rows whose (row, KV head) segment was cut between workers: combine the
-// partials o = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w. Rows without
-// context get zeros; segments a single worker covered were written directly.
-// One wave per (row, query head): lanes take 64 partials' (m, l) at a time,
-// then every lane folds two head dims over the partials with eight loads in
-// flight. (Merging inside the decode kernel instead would need device-scope
-// release/acquire between workgroups, which on this chip writes back and
-// invalidates a whole L2 per segment; the kernel boundary is far cheaper.)
+// Segments cut between workers: o = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w -
+// M) l_w over the partials of workers w0 .. w1. The decode kernel's worker
+// w0 (the one that started the segment and left it unfinished) named the
+// segment in its entry of the cut list; every other entry is -1, so the merge
+// grid has one wave per worker and most waves return after one load. Segments
+// a single worker covered were written directly, and rows without context
+// were written as zeros by that worker (a worker that sees no tile of a row
+// never runs for it: rows without context have no tiles, so they are written
+// here). The G heads of the segment share the wave: 64 / G lanes per head,
+// each folding 2 G of its head's dims, eight partials in flight. (Merging
+// inside the decode kernel instead would need device-scope release/acquire
+// between workgroups, which on this chip writes back and invalidates a whole
+// L2 per segment; the kernel boundary is far cheaper.)
 constexpr int kMergeWaves = 4;
 
-__global__ __launch_bounds__(kMergeWaves * kWave) void decode_mfma_merge_kernel(DecodeArgs a, int group) {
+template <int G>
+__global__ __launch_bounds__(kMergeWaves * kWave) void decode_mfma_merge_kernel(DecodeArgs a) {
+  constexpr int L = kWave / G;          // lanes per head
+  constexpr int DPL = kHeadDim / L;     // dims per lane (2 G)
   const int lane = threadIdx.x & (kWave - 1);
   const int item = blockIdx.x * kMergeWaves + wave_id_uniform();
-  if (item >= a.num_rows * a.num_q_heads) return;
-  const int hq = item % a.num_q_heads;
-  const int row = item / a.num_q_heads;
-  const int g = hq / group, hl = hq - g * group;
-  int s, ctx;
-  resolve_row(a, row, s, ctx);
-  uint32_t* out = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.out) + ((size_t)row * a.num_q_heads + hq) * kHeadDim) + lane;
-  if (ctx <= 0) {
-    *out = 0u;
-    return;
+  // Rows without context have no tiles, so no worker saw them: zeros.
+  if (item < a.num_rows) {
+    int s0, ctx0;
+    resolve_row(a, item, s0, ctx0);
+    if (ctx0 <= 0) {
+      uint32_t* z = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.out) + (size_t)item * a.num_q_heads * kHeadDim);
+      for (int i = lane; i < a.num_q_heads * kHeadDim / 2; i += kWave) z[i] = 0u;
+    }
   }
-  const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
   const int total = a.ws_rows[a.num_rows];
   const int workers = min(a.num_workers, total);
+  if (item >= workers) return;
+  const int code = a.ws_cut[item];
+  if (code < 0) return;
+  const int nkv = a.num_kv_heads;
+  const int row = __builtin_amdgcn_readfirstlane(code / nkv);
+  const int g = __builtin_amdgcn_readfirstlane(code - (code / nkv) * nkv);
+  int s, ctx;
+  resolve_row(a, row, s, ctx);
+  const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
   const int64_t first_tile = (int64_t)a.ws_rows[row] + (int64_t)g * nblk;
-  const int w0 = __builtin_amdgcn_readfirstlane(worker_of(first_tile, total, workers));
+  const int w0 = item;
   const int w1 = __builtin_amdgcn_readfirstlane(worker_of(first_tile + nblk - 1, total, workers));
-  if (w0 == w1) return;
-  const size_t seg = (size_t)row * a.num_kv_heads + g;
-
+  const int hl = lane / L, sub = lane % L;
+  const size_t seg = (size_t)row * nkv + g;
+  // the head's max over the partials (lanes of the head take every L-th one)
   float M = kNoMax;
-  for (int c = w0; c <= w1; c += kWave) {
-    const int w = c + lane;
-    if (w <= w1) M = fmaxf(M, a.ws_ml[2 * ((seg + w) * group + hl)]);
-  }
-  M = wave_max(M);
-  float L = 0.0f, Ax = 0.0f, Ay = 0.0f;
-  for (int c = w0; c <= w1; c += kWave) {
-    const int w = c + lane;
+  for (int w = w0 + sub; w <= w1; w += L) M = fmaxf(M, a.ws_ml[2 * ((seg + w) * G + hl)]);
+#pragma unroll
+  for (int o = L / 2; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  float Lsum = 0.0f;
+  float acc[DPL];
+#pragma unroll
+  for (int d = 0; d < DPL; ++d) acc[d] = 0.0f;
+  for (int c = w0; c <= w1; c += L) {
+    // lane sub holds the weight of partial c + sub of its head
     float wt = 0.0f;
-    if (w <= w1) {
-      const size_t slot = (seg + w) * group + hl;
+    if (c + sub <= w1) {
+      const size_t slot = (seg + c + sub) * G + hl;
       wt = fast_exp2(a.ws_ml[2 * slot] - M);
-      L = fmaf(a.ws_ml[2 * slot + 1], wt, L);
+      Lsum = fmaf(a.ws_ml[2 * slot + 1], wt, Lsum);
     }
-    const int cnt = min(kWave, w1 - c + 1);
+    const int cnt = min(L, w1 - c + 1);
     for (int j0 = 0; j0 < cnt; j0 += 8) {
-      float2 v[8];
+      float2 v[8][DPL / 2];
       float wj[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {   // indices clamped in range; padding gets weight 0
         const int j = min(j0 + u, cnt - 1);
-        wj[u] = (j0 + u < cnt) ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wt), j)) : 0.0f;
-        v[u] = reinterpret_cast<const float2*>(a.ws_acc + ((seg + c + j) * group + hl) * kHeadDim)[lane];
+        const float w = __shfl(wt, hl * L + j);
+        wj[u] = (j0 + u < cnt) ? w : 0.0f;
+        const float2* src = reinterpret_cast<const float2*>(a.ws_acc + ((seg + c + j) * G + hl) * kHeadDim + sub * DPL);
+#pragma unroll
+        for (int q = 0; q < DPL / 2; ++q) v[u][q] = src[q];
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        Ax = fmaf(v[u].x, wj[u], Ax);
-        Ay = fmaf(v[u].y, wj[u], Ay);
+#pragma unroll
+        for (int q = 0; q < DPL / 2; ++q) {
+          acc[2 * q] = fmaf(v[u][q].x, wj[u], acc[2 * q]);
+          acc[2 * q + 1] = fmaf(v[u][q].y, wj[u], acc[2 * q + 1]);
+        }
       }
     }
   }
-  L = wave_sum(L);
-  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  *out = pack2_bf16(Ax * inv, Ay * inv);
+#pragma unroll
+  for (int o = L / 2; o >= 1; o >>= 1) Lsum += __shfl_xor(Lsum, o);
+  const float inv = Lsum > 0.0f ? 1.0f / Lsum : 0.0f;
+  uint32_t* out = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.out) +
+                                              ((size_t)row * a.num_q_heads + g * G + hl) * kHeadDim + sub * DPL);
+#pragma unroll
+  for (int d = 0; d < DPL; d += 2) out[d / 2] = pack2_bf16(acc[d] * inv, acc[d + 1] * inv);
 }
 
 }  // namespace
@@ -536,8 +567,10 @@ hipError_t launch_group(DecodeArgs a, hipStream_t stream, int slot) {
   hipLaunchKernelGGL((decode_mfma_kernel<G>), dim3(grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const unsigned merge_grid = (unsigned)(((long long)a.num_rows * a.num_q_heads + kMergeWaves - 1) / kMergeWaves);
-  hipLaunchKernelGGL(decode_mfma_merge_kernel, dim3(merge_grid), dim3(kMergeWaves * kWave), 0, stream, a, G);
+  // one wave per worker (its cut-list entry) and per row (rows without context)
+  const long long items = a.num_workers > a.num_rows ? a.num_workers : a.num_rows;
+  const unsigned merge_grid = (unsigned)((items + kMergeWaves - 1) / kMergeWaves);
+  hipLaunchKernelGGL(decode_mfma_merge_kernel<G>, dim3(merge_grid), dim3(kMergeWaves * kWave), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -560,7 +593,7 @@ size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max
     const int gmax = num_q_heads < 8 ? num_q_heads : 8;
     const size_t slots = (size_t)num_rows * num_q_heads + (size_t)kWaves * kMaxDecodeGrid * gmax;
     return round_up_256(((size_t)num_rows + 1) * sizeof(int32_t)) + round_up_256(slots * kHeadDim * sizeof(float)) +
-           slots * 2 * sizeof(float);
+           round_up_256(slots * 2 * sizeof(float)) + (size_t)kWaves * kMaxDecodeGrid * sizeof(int32_t);
   }
   const DecodePlan p = plan_decode(num_rows, max_ctx);
   if (p.n_split_max <= 1) return 0;
@@ -576,9 +609,11 @@ void set_decode_workspace(DecodeArgs& a, void* ws, bool bf16) {
     a.ws_rows = reinterpret_cast<int32_t*>(base);
     a.ws_acc = reinterpret_cast<float*>(base + round_up_256(((size_t)a.num_rows + 1) * sizeof(int32_t)));
     a.ws_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(a.ws_acc) + round_up_256(slots * kHeadDim * sizeof(float)));
+    a.ws_cut = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(a.ws_ml) + round_up_256(slots * 2 * sizeof(float)));
     return;
   }
   a.ws_rows = nullptr;
+  a.ws_cut = nullptr;
   a.ws_acc = reinterpret_cast<float*>(base);
   a.ws_ml = base ? a.ws_acc + (size_t)a.num_rows * a.num_q_heads * a.n_split_max * kHeadDim : nullptr;
 }
