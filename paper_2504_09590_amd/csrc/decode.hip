@@ -215,17 +215,34 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const int blk = load_uniform(a.block_tables, (size_t)c.s * a.max_blocks_per_seq + c.b);
     return (blk >= 0 && blk < a.num_blocks) ? blk : -1;
   };
-  auto issue_k = [&](v4u_t (&kf)[4], int blk, int g) {
-    if (blk < 0) return;
-    const size_t base = ((size_t)blk * nkv + g) * kTileElems + k_lane;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) kf[c] = load_nt(a.k_pool, base + 32 * c);
+  // Slots of tile c that hold context: all 16, except in a tail block, where
+  // they are [0, r) walking from the left and [16 - r, 16) from the right.
+  // The rows of the other slots are not loaded (their scores and V rows are
+  // dropped by selection in the tile's body whatever the registers hold).
+  auto slot_lo = [&](const Cursor& c) -> int {
+    const int r = c.ctx & (kBlockSize - 1);
+    return (c.b == c.nblk - 1 && r != 0 && c.dirv < 0) ? kBlockSize - r : 0;
   };
-  auto issue_v = [&](v4u_t (&vf)[4], int blk, int g) {
+  auto slot_hi = [&](const Cursor& c) -> int {
+    const int r = c.ctx & (kBlockSize - 1);
+    return (c.b == c.nblk - 1 && r != 0 && c.dirv > 0) ? r : kBlockSize;
+  };
+  auto issue_k = [&](v4u_t (&kf)[4], int blk, const Cursor& c) {
     if (blk < 0) return;
-    const size_t base = ((size_t)blk * nkv + g) * kTileElems + v_lane;
+    if (col < slot_lo(c) || col >= slot_hi(c)) return;   // this lane's K row is slot col
+    const size_t base = ((size_t)blk * nkv + c.g) * kTileElems + k_lane;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) vf[j] = load_nt(a.v_pool, base + (size_t)j * kHeadDim);
+    for (int k = 0; k < 4; ++k) kf[k] = load_nt(a.k_pool, base + 32 * k);
+  };
+  auto issue_v = [&](v4u_t (&vf)[4], int blk, const Cursor& c) {
+    if (blk < 0) return;
+    const int lo = slot_lo(c), hi = slot_hi(c);
+    const size_t base = ((size_t)blk * nkv + c.g) * kTileElems + v_lane;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int slot = 4 * grp + j;   // this lane's V rows
+      if (slot >= lo && slot < hi) vf[j] = load_nt(a.v_pool, base + (size_t)j * kHeadDim);
+    }
   };
   auto load_q = [&](const Cursor& c) {
     const size_t qoff = ((size_t)c.row * Hq + c.g * G + col) * kHeadDim + 8 * grp;
@@ -241,8 +258,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   int blk[kDepth + 2];
   locate(a, s_pre, chunk, nch, t0, cur[0]);
   blk[0] = table(cur[0]);
-  issue_k(kf_[0], blk[0], cur[0].g);
-  issue_v(vf_[0], blk[0], cur[0].g);
+  issue_k(kf_[0], blk[0], cur[0]);
+  issue_v(vf_[0], blk[0], cur[0]);
   load_q(cur[0]);
   bool whole = cur[0].b == 0;   // this wave saw the segment's first tile
 #pragma unroll
@@ -253,8 +270,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       advance(a, cur[d]);
       blk[d] = table(cur[d]);
       if (d < kDepth) {
-        issue_k(kf_[d], blk[d], cur[d].g);
-        issue_v(vf_[d], blk[d], cur[d].g);
+        issue_k(kf_[d], blk[d], cur[d]);
+        issue_v(vf_[d], blk[d], cur[d]);
       }
     }
   }
@@ -290,7 +307,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
     // K and query registers are free: keys kDepth tiles ahead (and the query
     // of the next tile's segment)
-    if (i + kDepth < n) issue_k(kf, blk[kDepth], cur[kDepth].g);
+    if (i + kDepth < n) issue_k(kf, blk[kDepth], cur[kDepth]);
     if (i + 1 < n && seg_end) load_q(cur[1]);
     if (blk0 >= 0) {
       float s[4];
@@ -335,7 +352,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       }
     }
     // V registers are free: values kDepth tiles ahead
-    if (i + kDepth < n) issue_v(vf, blk[kDepth], cur[kDepth].g);
+    if (i + kDepth < n) issue_v(vf, blk[kDepth], cur[kDepth]);
 
     if (seg_end) {
       // The four lane groups of a head hold disjoint slots: total their weights.
