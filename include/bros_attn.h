@@ -287,9 +287,13 @@ int bros_kv_scatter(const void* k_in, const void* v_in,
  * bros_copy_dma -- an asynchronous copy of `bytes` bytes on a DMA engine.
  *
  * Defines: the host copies of Sec. 5.2's lazy checkpointing, carried on their
- * own streams (Sec. 6). The copy runs on a copy engine, not on compute units,
- * so it proceeds beside kernels that occupy every compute unit (a copy made
- * as a kernel would queue behind them or take units from them). dst and src
+ * own streams (Sec. 6). The copy is requested as one that needs no compute
+ * unit (hipMemcpyDeviceToDeviceNoCU), so that it can proceed beside kernels
+ * that occupy every compute unit. Whether a copy engine performs it is the
+ * HIP runtime's choice: the ROCm 7.2 runtime uses one, while the runtime
+ * bundled with PyTorch for ROCm 7.0 performs such copies as kernels
+ * (__amd_rocclr_copyBuffer), which then queue behind or share compute units
+ * with the attention kernels. dst and src
  * are device memory or pinned host memory (hipHostMalloc, or torch's
  * pin_memory); the ranges must not overlap. Enqueued on `stream`; returns
  * BROS_OK, BROS_E_NULL (a NULL pointer with bytes > 0) or BROS_E_HIP.
@@ -306,6 +310,25 @@ int bros_copy_dma(void* dst, const void* src, size_t bytes, void* stream);
  * BROS_E_SHAPE for bad arguments).
  */
 int bros_check_slot_ids(const int32_t* slot_ids, int32_t num_slots, int32_t num_blocks);
+
+/*
+ * bros_slot_ids -- slot ids of chosen (sequence, logical position) pairs.
+ *
+ * Defines: the slot mapping of Sec. 5.1 with the exclusive view of Sec. 5.2,
+ * the one every kernel applies: position p of sequence s lives in block
+ * block_tables[s][p / 16], slot p % 16 when its entry walks from the left
+ * (+1) and 15 - p % 16 from the right (-1); the id is block * 16 + slot.
+ * For i in [0, n): slot_ids[i] = id of (seqs[i], positions[i]). Directions
+ * as in COMMON CONVENTIONS (dir per sequence, per table entry when
+ * dir_per_entry is 1, or from cls when dir is NULL). All pointers are HOST
+ * pointers; slot_ids is written by the caller-owned array of n entries.
+ * Errors: BROS_E_NULL, BROS_E_SHAPE (bad counts), BROS_E_TABLE (a sequence
+ * index outside [0, num_seqs), a position beyond the table, an entry outside
+ * [0, num_blocks), a flag other than +1 / -1), naming the first bad pair.
+ */
+int bros_slot_ids(const int32_t* block_tables, int32_t max_blocks_per_seq, const int8_t* dir,
+                  const uint8_t* cls, int32_t dir_per_entry, int32_t num_seqs, int32_t num_blocks,
+                  const int32_t* seqs, const int32_t* positions, int32_t n, int32_t* slot_ids);
 
 /*
  * bros_stream_create_cu_share -- a stream whose kernels run on a fixed share

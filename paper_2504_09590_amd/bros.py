@@ -26,7 +26,7 @@ STATUS = {0: "BROS_OK", -1: "BROS_E_NULL", -2: "BROS_E_SHAPE", -3: "BROS_E_DTYPE
 EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_write",
             "bros_attn_decode", "bros_attn_decode_noalloc", "bros_attn_prefill_chunk", "bros_attn_workspace_size",
             "bros_check_batch", "bros_stream_create_cu_share", "bros_stream_destroy",
-            "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma",
+            "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma", "bros_slot_ids",
             "bros_mgr_create", "bros_mgr_destroy", "bros_mgr_add_request", "bros_mgr_release", "bros_mgr_grow",
             "bros_mgr_restore", "bros_mgr_query", "bros_mgr_table", "bros_mgr_free_blocks", "bros_mgr_validate", "bros_mgr_available",
             "bros_mgr_entries_needed", "bros_mgr_preemption_table", "bros_schedule", "bros_next_batch_size"]
@@ -75,6 +75,8 @@ def _load() -> ctypes.CDLL:
     lib.bros_kv_scatter.restype = ctypes.c_int
     lib.bros_check_slot_ids.argtypes = [P, I, I]
     lib.bros_check_slot_ids.restype = ctypes.c_int
+    lib.bros_slot_ids.argtypes = [P, I, P, P, I, I, I, P, P, I, P]
+    lib.bros_slot_ids.restype = ctypes.c_int
     lib.bros_copy_dma.argtypes = [P, P, Z, P]
     lib.bros_copy_dma.restype = ctypes.c_int
     from . import manager as _m   # host block manager and scheduler signatures
@@ -220,6 +222,22 @@ def bros_copy_dma(dst, src, nbytes: int | None = None, stream=None) -> None:
     if n > dst.numel() * dst.element_size() or n > src.numel() * src.element_size():
         raise ValueError("copy larger than a buffer")
     _check(LIB.bros_copy_dma(_ptr(dst), _ptr(src), n, _stream(stream)))
+
+
+def bros_slot_ids(block_tables: np.ndarray, dir, cls, num_blocks: int, seqs, positions) -> np.ndarray:
+    """Host: slot ids (block * 16 + slot) of (sequence, position) pairs under
+    the batch's tables and directions; raises BrosError naming a bad pair."""
+    bt = np.ascontiguousarray(block_tables, dtype=np.int32)
+    dr = None if dir is None else np.ascontiguousarray(dir, dtype=np.int8)
+    cs = None if cls is None else np.ascontiguousarray(cls, dtype=np.uint8)
+    sq = np.ascontiguousarray(seqs, dtype=np.int32)
+    ps = np.ascontiguousarray(positions, dtype=np.int32)
+    if sq.shape != ps.shape:
+        raise ValueError("seqs and positions must have the same length")
+    out = np.empty(sq.shape[0], dtype=np.int32)
+    _check(LIB.bros_slot_ids(_ptr(bt), int(bt.shape[1]), _ptr(dr), _ptr(cs), _dir_mode(dr, bt), int(bt.shape[0]),
+                             int(num_blocks), _ptr(sq), _ptr(ps), int(sq.shape[0]), _ptr(out)))
+    return out
 
 
 def bros_check_slot_ids(slot_ids: np.ndarray, num_blocks: int) -> None:

@@ -93,3 +93,39 @@ extern "C" int bros_check_slot_ids(const int32_t* slot_ids, int32_t num_slots, i
   }
   return bros::ok();
 }
+
+// Slot ids (block * 16 + slot) of chosen (sequence, logical position) pairs,
+// with the mapping every kernel uses: entry p / 16 of the sequence's table and
+// slot p % 16 walking from the left, 15 - p % 16 from the right (Sec. 5.1,
+// with the exclusive view of Sec. 5.2).
+extern "C" int bros_slot_ids(const int32_t* block_tables, int32_t max_blocks_per_seq, const int8_t* dir,
+                             const uint8_t* cls, int32_t dir_per_entry, int32_t num_seqs, int32_t num_blocks,
+                             const int32_t* seqs, const int32_t* positions, int32_t n, int32_t* slot_ids) {
+  if (num_seqs < 0 || max_blocks_per_seq <= 0 || num_blocks <= 0 || n < 0)
+    return fail(BROS_E_SHAPE, "bad counts: num_seqs=%d max_blocks_per_seq=%d num_blocks=%d n=%d", num_seqs,
+                max_blocks_per_seq, num_blocks, n);
+  if (n == 0) return bros::ok();
+  if (!block_tables || !seqs || !positions || !slot_ids) return fail(BROS_E_NULL, "a table, list or output pointer is NULL");
+  if (!dir && !cls) return fail(BROS_E_NULL, "dir and cls are both NULL");
+  if (dir_per_entry != 0 && dir_per_entry != 1) return fail(BROS_E_SHAPE, "dir_per_entry %d is neither 0 nor 1", dir_per_entry);
+  if (dir_per_entry && !dir) return fail(BROS_E_NULL, "dir_per_entry is set but dir is NULL");
+  for (int32_t i = 0; i < n; ++i) {
+    const int s = seqs[i], p = positions[i];
+    if (s < 0 || s >= num_seqs) return fail(BROS_E_TABLE, "pair %d: sequence %d outside [0, %d)", i, s, num_seqs);
+    if (p < 0 || p / 16 >= max_blocks_per_seq)
+      return fail(BROS_E_TABLE, "pair %d: position %d beyond the %d table entries", i, p, max_blocks_per_seq);
+    const int32_t id = block_tables[(size_t)s * max_blocks_per_seq + p / 16];
+    if (id < 0 || id >= num_blocks)
+      return fail(BROS_E_TABLE, "pair %d: sequence %d entry %d = %d outside [0, %d)", i, s, p / 16, id, num_blocks);
+    int d;
+    if (!dir) {
+      d = cls[s] == 1 ? -1 : 1;
+    } else {
+      d = dir_per_entry ? dir[(size_t)s * max_blocks_per_seq + p / 16] : dir[s];
+      if (d != 1 && d != -1) return fail(BROS_E_TABLE, "pair %d: direction flag %d is not +1 or -1", i, d);
+    }
+    const int off = p % 16;
+    slot_ids[i] = id * 16 + (d > 0 ? off : 15 - off);
+  }
+  return bros::ok();
+}

@@ -86,19 +86,18 @@ class MixedStep:
 
     def _init_swap(self, n: int):
         b, d = self.batch, self.dev
-        ids = []
+        # early positions of the decode sequences, which no write of the step touches
+        seqs, pos = [], []
         for depth in range(int(b.ctx_lens.max())):
             for s in range(self.P, self.S):
-                if depth < int(b.ctx_lens[s]) - 1 and len(ids) < n:
-                    # slot of logical position `depth` (Sec. 5.1: RT from the left, BE from the right)
-                    off = depth % 16
-                    slot = off if int(b.dir[s]) > 0 else 15 - off
-                    ids.append(int(b.block_tables[s][depth // 16]) * 16 + slot)
-            if len(ids) >= n:
+                if depth < int(b.ctx_lens[s]) - 1 and len(seqs) < n:
+                    seqs.append(s)
+                    pos.append(depth)
+            if len(seqs) >= n:
                 break
-        if len(ids) < n:
+        if len(seqs) < n:
             raise ValueError(f"the batch's decode sequences hold fewer than {n} untouched slots")
-        ids = np.asarray(ids, dtype=np.int32)
+        ids = bros.bros_slot_ids(b.block_tables, b.dir, b.cls, b.num_blocks, seqs, pos)
         bros.bros_check_slot_ids(ids, b.num_blocks)
         self.swap_ids = torch.from_numpy(ids).to(d.k_pool.device)
         hkv, hd = d.k_pool.shape[1], d.k_pool.shape[3]

@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings_and_version():
     for code, name in bros.STATUS.items():
         assert bros.LIB.bros_status_str(code).decode() == name
-    assert bros.LIB.bros_abi_version() == 7
+    assert bros.LIB.bros_abi_version() == 8
 
 
 # --- argument validation (returns before any HIP call) -----------------------
@@ -290,3 +290,24 @@ def test_noalloc_decode_rejects_a_batch_beyond_its_scratch_array():
     st = bros.LIB.bros_attn_decode_noalloc(None, None, None, None, 10, None, 4, None, None, 0, None, 64, 2,
                                            32, 8, 128, 16, 0.0, bros.BROS_BF16, None)
     assert st == -1
+
+
+def test_slot_ids_follow_the_oracle_mapping():
+    # The library's slot ids of (sequence, position) pairs equal the oracle's
+    # own (block, slot) mapping, per-sequence and per-entry directions alike.
+    b = W.custom([40, 17, 70, 9, 33], [W.RT, W.BE, W.BE, W.RT, W.RT], 8, 4, seed=41, spare_blocks=5)
+    rng = np.random.default_rng(41)
+    seqs = rng.integers(0, b.num_seqs, 200)
+    pos = np.array([rng.integers(0, b.ctx_lens[s]) for s in seqs])
+    for dirs in (b.dir, np.where(rng.random(b.block_tables.shape) < 0.5, 1, -1).astype(np.int8)):
+        got = bros.bros_slot_ids(b.block_tables, dirs, b.cls, b.num_blocks, seqs, pos)
+        for i, (s, p) in enumerate(zip(seqs, pos)):
+            blk, slot = oracle.physical_location(b.block_tables, dirs, int(s), [int(p)])
+            assert got[i] == int(blk[0]) * 16 + int(slot[0])
+    # direction from the class when dir is NULL
+    got = bros.bros_slot_ids(b.block_tables, None, b.cls, b.num_blocks, seqs, pos)
+    assert np.array_equal(got, bros.bros_slot_ids(b.block_tables, b.dir, None, b.num_blocks, seqs, pos))
+    with pytest.raises(bros.BrosError, match="outside"):
+        bros.bros_slot_ids(b.block_tables, b.dir, b.cls, b.num_blocks, [b.num_seqs], [0])
+    with pytest.raises(bros.BrosError, match="beyond"):
+        bros.bros_slot_ids(b.block_tables, b.dir, b.cls, b.num_blocks, [0], [16 * b.block_tables.shape[1]])
