@@ -424,6 +424,25 @@ int bros_mgr_release(void* mgr, int32_t req);             /* frees its slots; dr
 int bros_mgr_grow(void* mgr, int32_t req, int32_t n_new, bros_mgr_plan* plan);
 /* Brings req's checkpointed tokens back: moves and restore destinations. */
 int bros_mgr_restore(void* mgr, int32_t req, bros_mgr_plan* plan);
+/* One call for a whole iteration's block management: for i in [0, n), in
+ * order, request reqs[i] is restored first when it has checkpointed tokens
+ * (restore_first = 1; with 0 such a request fails with BROS_E_TABLE) and
+ * then grown by n_new[i] tokens, as bros_mgr_restore and bros_mgr_grow do.
+ * The plan holds every request's lists concatenated in request order; ends
+ * (int32 [n][4], caller-owned) gives, after request i, the running counts of
+ * victims, moves, restores and written tokens, so request i's entries of each
+ * list are [ends[i-1][k], ends[i][k]). status[i] (int32 [n]) is BROS_OK or
+ * that request's error (BROS_E_NOMEM, BROS_E_TABLE); a failing request keeps
+ * what it placed before the failure and later requests still run. Returns
+ * BROS_OK, the first request's error, BROS_E_SHAPE (an unknown request or a
+ * negative count, checked before anything changes, or a plan buffer too
+ * small) or BROS_E_NULL. Host memory only. */
+int bros_mgr_grow_batch(void* mgr, const int32_t* reqs, const int32_t* n_new, int32_t n, int32_t restore_first,
+                        bros_mgr_plan* plan, int32_t* ends, int32_t* status);
+/* An entry count that every list of the plan of bros_mgr_grow_batch(reqs,
+ * n_new, n) stays within (plan buffers of this many entries, victims 4 times
+ * as many ints, never make it fail for want of room); -1 for bad arguments. */
+int32_t bros_mgr_plan_bound(void* mgr, const int32_t* reqs, const int32_t* n_new, int32_t n);
 int bros_mgr_query(void* mgr, int32_t req, int32_t* ctx, int32_t* num_entries, int32_t* checkpointed);
 int bros_mgr_table(void* mgr, int32_t req, int32_t* out, int32_t cap);
 int32_t bros_mgr_free_blocks(void* mgr);
@@ -465,6 +484,20 @@ typedef struct bros_cost_model {
 int bros_schedule(void* mgr, const bros_sched_req* rt, int32_t n_rt, const bros_sched_req* be, int32_t n_be,
                   int32_t batch_size, const bros_cost_model* cost, int32_t* rt_ready, int32_t* n_rt_ready,
                   int32_t* be_ready, int32_t* n_be_ready, int32_t* over_budget);
+/* Alg. 1 with Sec. 4.2's request pulling: the RT queue comes as the pending
+ * queue (any order) and the waiting queue, which the caller keeps in ascending
+ * order of remaining time (the paper: the waiting queue is ordered by arrival,
+ * so its head has waited longest). Only the pending queue is sorted, and only
+ * its first batch_size requests (a partial sort); the RT order is then pulled
+ * by polling the two queue heads and taking the more urgent one (pending
+ * first on ties). The BE queue is partially sorted as far as the BE loop can
+ * reach (2 batch_size + 1 requests). With a waiting queue in that order the
+ * result equals bros_schedule over the pending and waiting requests together
+ * (pending listed first). Same outputs and errors as bros_schedule. */
+int bros_schedule_pulled(void* mgr, const bros_sched_req* pending, int32_t n_pending, const bros_sched_req* waiting,
+                         int32_t n_waiting, const bros_sched_req* be, int32_t n_be, int32_t batch_size,
+                         const bros_cost_model* cost, int32_t* rt_ready, int32_t* n_rt_ready, int32_t* be_ready,
+                         int32_t* n_be_ready, int32_t* over_budget);
 /* Adaptive batch sizing: back to `base` after an over-budget iteration, else
  * doubled (at most max_size). */
 int32_t bros_next_batch_size(int32_t current, int32_t base, int32_t max_size, int32_t over_budget);

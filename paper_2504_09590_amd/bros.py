@@ -29,7 +29,8 @@ EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_w
             "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma", "bros_slot_ids",
             "bros_mgr_create", "bros_mgr_destroy", "bros_mgr_add_request", "bros_mgr_release", "bros_mgr_grow",
             "bros_mgr_restore", "bros_mgr_query", "bros_mgr_table", "bros_mgr_free_blocks", "bros_mgr_validate", "bros_mgr_available",
-            "bros_mgr_entries_needed", "bros_mgr_preemption_table", "bros_schedule", "bros_next_batch_size"]
+            "bros_mgr_entries_needed", "bros_mgr_preemption_table", "bros_schedule", "bros_next_batch_size",
+            "bros_mgr_grow_batch", "bros_mgr_plan_bound", "bros_schedule_pulled"]
 
 
 class BrosError(RuntimeError):

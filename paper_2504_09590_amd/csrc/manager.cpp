@@ -422,6 +422,60 @@ int bros_mgr_grow(void* mgr, int32_t req, int32_t n_new, bros_mgr_plan* plan) {
   return copy_plan(p, plan);
 }
 
+int bros_mgr_grow_batch(void* mgr, const int32_t* reqs, const int32_t* n_new, int32_t n, int32_t restore_first,
+                        bros_mgr_plan* plan, int32_t* ends, int32_t* status) {
+  const char* fn = "bros_mgr_grow_batch";
+  if (!mgr) return fail(BROS_E_NULL, "%s: mgr is NULL", fn);
+  if (n < 0) return fail(BROS_E_SHAPE, "%s: n %d", fn, n);
+  if (n > 0 && (!reqs || !n_new || !ends || !status)) return fail(BROS_E_NULL, "%s: NULL list", fn);
+  Manager* m = as_mgr(mgr);
+  for (int32_t i = 0; i < n; ++i) {   // arguments first: nothing changes for a bad call
+    if (!m->has(reqs[i])) return fail(BROS_E_SHAPE, "%s: no request %d (index %d)", fn, reqs[i], i);
+    if (n_new[i] < 0) return fail(BROS_E_SHAPE, "%s: n_new %d (index %d)", fn, n_new[i], i);
+  }
+  Plan p;
+  int first_err = BROS_OK, first_idx = -1;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t req = reqs[i];
+    int st = BROS_OK;
+    if (m->req(req).checkpointed() > 0) {
+      if (!restore_first) st = BROS_E_TABLE;
+      else if (!m->restore(req, p)) st = BROS_E_NOMEM;
+    }
+    for (int32_t k = 0; st == BROS_OK && k < n_new[i]; ++k)
+      if (!m->grow_one(req, p)) st = BROS_E_NOMEM;
+    status[i] = st;
+    if (st != BROS_OK && first_err == BROS_OK) {
+      first_err = st;
+      first_idx = i;
+    }
+    ends[4 * i + 0] = (int32_t)(p.victims.size() / 4);
+    ends[4 * i + 1] = (int32_t)p.move_src.size();
+    ends[4 * i + 2] = (int32_t)p.restore_pos.size();
+    ends[4 * i + 3] = (int32_t)p.written.size();
+  }
+  const int cst = copy_plan(p, plan);
+  if (cst != BROS_OK) return cst;
+  if (first_err != BROS_OK)
+    return fail(first_err, "%s: request %d (index %d) %s; the other requests' results are in the plan", fn,
+                reqs[first_idx], first_idx,
+                first_err == BROS_E_NOMEM ? "found no block" : "has checkpointed tokens and restore_first is 0");
+  return bros::ok();
+}
+
+int32_t bros_mgr_plan_bound(void* mgr, const int32_t* reqs, const int32_t* n_new, int32_t n) {
+  if (!mgr || n < 0 || (n > 0 && (!reqs || !n_new))) return -1;
+  Manager* m = as_mgr(mgr);
+  int64_t cap = 64;
+  for (int32_t i = 0; i < n; ++i) {
+    if (!m->has(reqs[i]) || n_new[i] < 0) return -1;
+    // a new token victimises at most one peer token and a relocation moves at
+    // most 15; a restore moves or restores at most the request's tokens
+    cap += 16 * (int64_t)n_new[i] + m->req(reqs[i]).ctx + 16;
+  }
+  return cap > 0x7fffffff ? -1 : (int32_t)cap;
+}
+
 int bros_mgr_restore(void* mgr, int32_t req, bros_mgr_plan* plan) {
   if (!mgr) return fail(BROS_E_NULL, "bros_mgr_restore: mgr is NULL");
   Manager* m = as_mgr(mgr);
@@ -510,34 +564,32 @@ struct CostSums {
   }
 };
 
-int bros_schedule(void* mgr, const bros_sched_req* rt, int32_t n_rt, const bros_sched_req* be, int32_t n_be,
-                  int32_t batch_size, const bros_cost_model* cost, int32_t* rt_ready, int32_t* n_rt_ready,
-                  int32_t* be_ready, int32_t* n_be_ready, int32_t* over_budget) {
-  const char* fn = "bros_schedule";
-  if (!mgr || !cost || !rt_ready || !n_rt_ready || !be_ready || !n_be_ready || !over_budget)
-    return fail(BROS_E_NULL, "%s: NULL argument", fn);
-  if ((n_rt > 0 && !rt) || (n_be > 0 && !be) || n_rt < 0 || n_be < 0 || batch_size < 0)
-    return fail(BROS_E_SHAPE, "%s: bad queue arguments", fn);
-  Manager* m = as_mgr(mgr);
-  // RT queue in ascending remaining time; T_res_min is the most urgent's.
-  std::vector<const bros_sched_req*> qrt, qbe;
-  for (int32_t i = 0; i < n_rt; ++i) qrt.push_back(&rt[i]);
-  for (int32_t i = 0; i < n_be; ++i) qbe.push_back(&be[i]);
-  std::stable_sort(qrt.begin(), qrt.end(), [](auto a, auto b) { return a->remaining_us < b->remaining_us; });
-  std::stable_sort(qbe.begin(), qbe.end(), [](auto a, auto b) { return a->m_cpu < b->m_cpu; });
+}  // extern "C"
+
+namespace {
+
+// Alg. 1 over RT requests already in ascending order of remaining time (qrt)
+// and BE requests in ascending order of checkpointed slots (qbe). The RT loop
+// reads at most batch_size entries of qrt and the BE loop at most
+// 2 batch_size + 1 of qbe (each BE step adds one request to the batch or
+// replaces one RT request, else stops), so callers may pass only those
+// prefixes.
+int schedule_ordered(Manager* m, const std::vector<const bros_sched_req*>& qrt,
+                     const std::vector<const bros_sched_req*>& qbe, int32_t batch_size, const bros_cost_model* cost,
+                     int32_t* rt_ready, int32_t* n_rt_ready, int32_t* be_ready, int32_t* n_be_ready,
+                     int32_t* over_budget) {
   const double t_res = qrt.empty() ? std::numeric_limits<double>::infinity() : qrt.front()->remaining_us;
   // Blocks the batch may still take (FindPreemptBlock / FindBlock): free ones
   // first, then RT may take blocks without an RT owner (preempting BE) and BE
   // blocks without a BE owner that have an empty slot.
   int32_t free_left = m->free_blocks();
   int32_t open_left[2] = {m->open_for(BROS_RT), m->open_for(BROS_BE)};
-  auto need_of = [&](const bros_sched_req* r, int32_t cls) -> int32_t {
+  auto need_of = [&](const bros_sched_req* r) -> int32_t {
     if (!m->has(r->id)) return (r->ctx_after + kBS - 1) / kBS;
     const Request& q = m->req(r->id);
     int32_t moved = 0;   // entries with checkpointed tokens may move on restore
     if (q.missing)
       for (size_t e = 0; e < q.table.size(); ++e) moved += q.on_gpu[e] < q.count(e);
-    (void)cls;
     return m->entries_needed(r->id, r->n_new) + moved;
   };
   auto take = [&](int32_t need, int32_t cls, bool commit) -> bool {
@@ -557,7 +609,7 @@ int bros_schedule(void* mgr, const bros_sched_req* rt, int32_t n_rt, const bros_
   while (head < qrt.size()) {
     const bros_sched_req* r = qrt[head];
     if ((int32_t)ready_rt.size() == batch_size) break;
-    const int32_t need = need_of(r, BROS_RT);
+    const int32_t need = need_of(r);
     if (!take(need, BROS_RT, false)) break;             // FindPreemptBlock fails
     CostSums cand = sums;
     cand.add(r, 1);
@@ -573,7 +625,7 @@ int bros_schedule(void* mgr, const bros_sched_req* rt, int32_t n_rt, const bros_
   size_t bhead = 0;
   while (bhead < qbe.size()) {
     const bros_sched_req* r = qbe[bhead];
-    const int32_t need = need_of(r, BROS_BE);
+    const int32_t need = need_of(r);
     if (!take(need, BROS_BE, false)) break;             // FindBlock fails
     auto fits = [&](const CostSums& base, size_t n_ready) {
       CostSums cand = base;
@@ -605,6 +657,77 @@ int bros_schedule(void* mgr, const bros_sched_req* rt, int32_t n_rt, const bros_
   *n_rt_ready = (int32_t)ready_rt.size();
   *n_be_ready = (int32_t)ready_be.size();
   return bros::ok();
+}
+
+// The first k requests of q (pointers) in ascending key order, ties by
+// position: a partial sort, O(n log k).
+template <typename Key>
+void first_k_sorted(std::vector<const bros_sched_req*>& q, size_t k, Key key) {
+  k = std::min(k, q.size());
+  const bros_sched_req* base = q.empty() ? nullptr : q.front();
+  auto less = [&](const bros_sched_req* a, const bros_sched_req* b) {
+    const auto ka = key(a), kb = key(b);
+    return ka < kb || (ka == kb && a < b);   // entries point into one array: address order is position order
+  };
+  (void)base;
+  std::partial_sort(q.begin(), q.begin() + k, q.end(), less);
+  q.resize(k);
+}
+
+}  // namespace
+
+extern "C" {
+
+int bros_schedule(void* mgr, const bros_sched_req* rt, int32_t n_rt, const bros_sched_req* be, int32_t n_be,
+                  int32_t batch_size, const bros_cost_model* cost, int32_t* rt_ready, int32_t* n_rt_ready,
+                  int32_t* be_ready, int32_t* n_be_ready, int32_t* over_budget) {
+  const char* fn = "bros_schedule";
+  if (!mgr || !cost || !rt_ready || !n_rt_ready || !be_ready || !n_be_ready || !over_budget)
+    return fail(BROS_E_NULL, "%s: NULL argument", fn);
+  if ((n_rt > 0 && !rt) || (n_be > 0 && !be) || n_rt < 0 || n_be < 0 || batch_size < 0)
+    return fail(BROS_E_SHAPE, "%s: bad queue arguments", fn);
+  // RT queue in ascending remaining time; T_res_min is the most urgent's.
+  std::vector<const bros_sched_req*> qrt, qbe;
+  for (int32_t i = 0; i < n_rt; ++i) qrt.push_back(&rt[i]);
+  for (int32_t i = 0; i < n_be; ++i) qbe.push_back(&be[i]);
+  std::stable_sort(qrt.begin(), qrt.end(), [](auto a, auto b) { return a->remaining_us < b->remaining_us; });
+  std::stable_sort(qbe.begin(), qbe.end(), [](auto a, auto b) { return a->m_cpu < b->m_cpu; });
+  return schedule_ordered(as_mgr(mgr), qrt, qbe, batch_size, cost, rt_ready, n_rt_ready, be_ready, n_be_ready,
+                          over_budget);
+}
+
+int bros_schedule_pulled(void* mgr, const bros_sched_req* pending, int32_t n_pending, const bros_sched_req* waiting,
+                         int32_t n_waiting, const bros_sched_req* be, int32_t n_be, int32_t batch_size,
+                         const bros_cost_model* cost, int32_t* rt_ready, int32_t* n_rt_ready, int32_t* be_ready,
+                         int32_t* n_be_ready, int32_t* over_budget) {
+  const char* fn = "bros_schedule_pulled";
+  if (!mgr || !cost || !rt_ready || !n_rt_ready || !be_ready || !n_be_ready || !over_budget)
+    return fail(BROS_E_NULL, "%s: NULL argument", fn);
+  if ((n_pending > 0 && !pending) || (n_waiting > 0 && !waiting) || (n_be > 0 && !be) || n_pending < 0 ||
+      n_waiting < 0 || n_be < 0 || batch_size < 0)
+    return fail(BROS_E_SHAPE, "%s: bad queue arguments", fn);
+  // Only the pending queue is sorted, and only as far as the batch can reach;
+  // the waiting queue is taken in its own order. Polling the two heads and
+  // pulling the more urgent one yields the RT order Alg. 1 consumes.
+  const size_t k = (size_t)batch_size;
+  std::vector<const bros_sched_req*> qp;
+  qp.reserve(n_pending);
+  for (int32_t i = 0; i < n_pending; ++i) qp.push_back(&pending[i]);
+  first_k_sorted(qp, k, [](const bros_sched_req* r) { return r->remaining_us; });
+  std::vector<const bros_sched_req*> qrt;
+  qrt.reserve(std::min(k, qp.size() + (size_t)n_waiting));
+  size_t ip = 0, iw = 0;
+  while (qrt.size() < k && (ip < qp.size() || iw < (size_t)n_waiting)) {
+    const bool take_pending =
+        iw >= (size_t)n_waiting || (ip < qp.size() && qp[ip]->remaining_us <= waiting[iw].remaining_us);
+    qrt.push_back(take_pending ? qp[ip++] : &waiting[iw++]);
+  }
+  std::vector<const bros_sched_req*> qbe;
+  qbe.reserve(n_be);
+  for (int32_t i = 0; i < n_be; ++i) qbe.push_back(&be[i]);
+  first_k_sorted(qbe, 2 * k + 1, [](const bros_sched_req* r) { return r->m_cpu; });
+  return schedule_ordered(as_mgr(mgr), qrt, qbe, batch_size, cost, rt_ready, n_rt_ready, be_ready, n_be_ready,
+                          over_budget);
 }
 
 int32_t bros_next_batch_size(int32_t current, int32_t base, int32_t max_size, int32_t over_budget) {

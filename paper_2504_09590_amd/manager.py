@@ -57,6 +57,11 @@ def declare(lib) -> None:
         "bros_schedule": ([P, ctypes.POINTER(SchedReq), I, ctypes.POINTER(SchedReq), I, I,
                            ctypes.POINTER(CostModelC), I32P, I32P, I32P, I32P, I32P], ctypes.c_int),
         "bros_next_batch_size": ([I, I, I, I], I),
+        "bros_mgr_grow_batch": ([P, I32P, I32P, I, I, ctypes.POINTER(_Plan), I32P, I32P], ctypes.c_int),
+        "bros_mgr_plan_bound": ([P, I32P, I32P, I], I),
+        "bros_schedule_pulled": ([P, ctypes.POINTER(SchedReq), I, ctypes.POINTER(SchedReq), I,
+                                  ctypes.POINTER(SchedReq), I, I, ctypes.POINTER(CostModelC), I32P, I32P, I32P,
+                                  I32P, I32P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -139,6 +144,32 @@ class BlockManager:
     def grow(self, req: int, n_new: int) -> Plan:
         return self._run(self._b.LIB.bros_mgr_grow, int(req), int(n_new), cap=max(64, 2 * int(n_new) + 64))
 
+    def grow_batch(self, reqs, n_new, restore_first: bool = True):
+        """One call for an iteration's block management (restore, then grow,
+        per request, in order). Returns (plan, ends, status): the concatenated
+        plan, the [n][4] running counts of victims, moves, restores and
+        written tokens after each request, and each request's status. A
+        failing request raises nothing here: its status says so."""
+        r = np.ascontiguousarray(reqs, dtype=np.int32)
+        k = np.ascontiguousarray(n_new, dtype=np.int32)
+        n = int(r.shape[0])
+        ends = np.zeros((max(n, 1), 4), dtype=np.int32)
+        status = np.zeros(max(n, 1), dtype=np.int32)
+        cap = int(self._b.LIB.bros_mgr_plan_bound(self.h, r.ctypes.data_as(I32P), k.ctypes.data_as(I32P), n))
+        if cap < 0:
+            raise self._b.BrosError(-2, "bros_mgr_plan_bound: an unknown request or a negative count")
+        bufs, plan = self._buffers(cap)
+        st = self._b.LIB.bros_mgr_grow_batch(self.h, r.ctypes.data_as(I32P), k.ctypes.data_as(I32P), n,
+                                             1 if restore_first else 0, ctypes.byref(plan),
+                                             ends.ctypes.data_as(I32P), status.ctypes.data_as(I32P))
+        if st not in (0, -7, -8):
+            self._b._check(st)
+        out = Plan(bufs["victims"][:4 * plan.num_victims].reshape(-1, 4).copy(),
+                   bufs["move_src"][:plan.num_moves].copy(), bufs["move_dst"][:plan.num_moves].copy(),
+                   bufs["restore_pos"][:plan.num_restores].copy(), bufs["restore_dst"][:plan.num_restores].copy(),
+                   bufs["written_pos"][:plan.num_written].copy(), bufs["written_slot"][:plan.num_written].copy())
+        return out, ends[:n].copy(), status[:n].copy()
+
     def restore(self, req: int) -> Plan:
         ctx, _, ck = self.query(req)
         return self._run(self._b.LIB.bros_mgr_restore, int(req), cap=max(64, ctx + 64))
@@ -201,14 +232,42 @@ def schedule(mgr: BlockManager, rt, be, batch_size: int, coef, per_request: bool
     return out_rt[:n_rt.value].tolist(), out_be[:n_be.value].tolist(), bool(over.value)
 
 
+def schedule_pulled(mgr: BlockManager, pending, waiting, be, batch_size: int, coef, per_request: bool = False):
+    """Alg. 1 with the request-pulling optimization (Sec. 4.2): pending RT
+    requests in any order, waiting RT requests in ascending remaining time,
+    BE requests. Arrays of SCHED_DTYPE. Returns (rt ids, be ids, over_budget)."""
+    b = mgr._b
+    arrs = [np.ascontiguousarray(q if len(q) else np.zeros(1, dtype=SCHED_DTYPE), dtype=SCHED_DTYPE)
+            for q in (pending, waiting, be)]
+    ptrs = [a.ctypes.data_as(ctypes.POINTER(SchedReq)) for a in arrs]
+    cm = CostModelC()
+    for ph in range(2):
+        for k in range(3):
+            cm.coef[ph][k] = float(coef[ph][k])
+    cm.per_request = 1 if per_request else 0
+    out_rt = np.zeros(max(len(pending) + len(waiting), 1), dtype=np.int32)
+    out_be = np.zeros(max(len(be), 1), dtype=np.int32)
+    n_rt, n_be, over = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    b._check(b.LIB.bros_schedule_pulled(mgr.h, ptrs[0], len(pending), ptrs[1], len(waiting), ptrs[2], len(be),
+                                        int(batch_size), ctypes.byref(cm), out_rt.ctypes.data_as(I32P),
+                                        ctypes.byref(n_rt), out_be.ctypes.data_as(I32P), ctypes.byref(n_be),
+                                        ctypes.byref(over)))
+    return out_rt[:n_rt.value].tolist(), out_be[:n_be.value].tolist(), bool(over.value)
+
+
 def next_batch_size(current: int, base: int, max_size: int, over_budget: bool) -> int:
     return int(_lib().LIB.bros_next_batch_size(int(current), int(base), int(max_size), 1 if over_budget else 0))
 
 
 def main(argv=None):
-    """Host cost of one iteration's scheduling and block management: Alg. 1
-    over every queued request, then one decode token per scheduled request
-    (FindBlock / FindPreemptBlock and lazy checkpoints), on one CPU thread."""
+    """Host cost of one iteration's scheduling and block management on one CPU
+    thread: Alg. 1 over every queued request, then one decode token for every
+    scheduled request (restores, FindBlock / FindPreemptBlock, lazy
+    checkpoints). Two arrangements: one C call per request with a full sort of
+    the RT queue (per_request), and the iteration's block management in one
+    batched C call with Sec. 4.2's request pulling (batched; the waiting RT
+    queue is kept in ascending remaining time and only the pending queue is
+    sorted)."""
     import argparse
     import json
     import time
@@ -219,50 +278,72 @@ def main(argv=None):
     ap.add_argument("--batch", type=int, default=256)
     ap.add_argument("--seed", type=int, default=0)
     args = ap.parse_args(argv)
-    rng = np.random.default_rng(args.seed)
-    mgr = BlockManager(args.blocks)
-    cls = {}
-    for rid in range(1, args.requests + 1):
-        c = 0 if rng.random() < 0.25 else 1
-        mgr.add(rid, c)
-        cls[rid] = c
-        try:
-            mgr.grow(rid, int(rng.integers(64, 1200)))
-        except Exception:
-            mgr.release(rid)
-            del cls[rid]
     coef = ((7.3e-3, 1.0e-5, 18.4), (8.8e-3, 6.5e-4, 23.7))   # the fitted per-request form (us)
-    t_sched, t_grow, n_sched = 0.0, 0.0, 0
-    for it in range(args.iterations):
-        ids = np.array(sorted(cls), dtype=np.int32)
-        q = np.zeros(len(ids), dtype=SCHED_DTYPE)
-        q["id"] = ids
-        q["n_new"] = 1
-        q["ctx_after"] = [mgr.query(int(r))[0] + 1 for r in ids]
-        is_rt = np.array([cls[int(r)] == 0 for r in ids])
-        q["remaining_us"] = rng.uniform(2e3, 5e4, len(ids))
-        q["m_cpu"] = [mgr.query(int(r))[2] for r in ids]
-        t0 = time.perf_counter()
-        got_rt, got_be, _ = schedule(mgr, q[is_rt], q[~is_rt], args.batch, coef, per_request=True)
-        t1 = time.perf_counter()
-        for rid in got_rt + got_be:
+    out = {"requests": args.requests, "blocks": args.blocks, "batch": args.batch, "iterations": args.iterations}
+    for mode in ("per_request", "batched"):
+        rng = np.random.default_rng(args.seed)
+        mgr = BlockManager(args.blocks)
+        cls = {}
+        for rid in range(1, args.requests + 1):
+            c = 0 if rng.random() < 0.25 else 1
+            mgr.add(rid, c)
+            cls[rid] = c
             try:
-                if mgr.query(rid)[2]:
-                    mgr.restore(rid)
-                mgr.grow(rid, 1)
+                mgr.grow(rid, int(rng.integers(64, 1200)))
             except Exception:
                 mgr.release(rid)
                 del cls[rid]
-        t2 = time.perf_counter()
-        t_sched += t1 - t0
-        t_grow += t2 - t1
-        n_sched += len(got_rt) + len(got_be)
-    k = args.iterations
-    print(json.dumps({"requests": len(cls), "blocks": args.blocks, "batch": args.batch, "iterations": k,
-                      "scheduled_per_iteration": round(n_sched / k, 1),
-                      "schedule_us_per_iteration": round(t_sched / k * 1e6, 1),
-                      "block_management_us_per_iteration": round(t_grow / k * 1e6, 1),
-                      "note": "one ctypes call per scheduled request for block management (Python call overhead included)"}))
+        t_sched, t_grow, n_sched = 0.0, 0.0, 0
+        for it in range(args.iterations):
+            ids = np.array(sorted(cls), dtype=np.int32)
+            q = np.zeros(len(ids), dtype=SCHED_DTYPE)
+            q["id"] = ids
+            q["n_new"] = 1
+            info = np.array([mgr.query(int(r)) for r in ids], dtype=np.int64).reshape(-1, 3)
+            q["ctx_after"] = info[:, 0] + 1
+            is_rt = np.array([cls[int(r)] == 0 for r in ids])
+            q["remaining_us"] = rng.uniform(2e3, 5e4, len(ids))
+            q["m_cpu"] = info[:, 2]
+            rt, be = q[is_rt], q[~is_rt]
+            n_pend = len(rt) // 4
+            pending = rt[:n_pend]
+            waiting = np.sort(rt[n_pend:], order="remaining_us", kind="stable")   # the queue's own order
+            t0 = time.perf_counter()
+            if mode == "per_request":
+                got_rt, got_be, _ = schedule(mgr, np.concatenate([pending, waiting]), be, args.batch, coef,
+                                             per_request=True)
+            else:
+                got_rt, got_be, _ = schedule_pulled(mgr, pending, waiting, be, args.batch, coef, per_request=True)
+            t1 = time.perf_counter()
+            run = got_rt + got_be
+            if mode == "per_request":
+                for rid in run:
+                    try:
+                        if mgr.query(rid)[2]:
+                            mgr.restore(rid)
+                        mgr.grow(rid, 1)
+                    except Exception:
+                        mgr.release(rid)
+                        del cls[rid]
+            else:
+                _, _, status = mgr.grow_batch(run, np.ones(len(run), dtype=np.int32))
+                for rid, st in zip(run, status):
+                    if st != 0:
+                        mgr.release(rid)
+                        del cls[rid]
+            t2 = time.perf_counter()
+            t_sched += t1 - t0
+            t_grow += t2 - t1
+            n_sched += len(run)
+            if mode == "batched" and it == 0:
+                mgr.validate()
+        k = args.iterations
+        out[mode] = {"scheduled_per_iteration": round(n_sched / k, 1),
+                     "schedule_us_per_iteration": round(t_sched / k * 1e6, 1),
+                     "block_management_us_per_iteration": round(t_grow / k * 1e6, 1),
+                     "total_us_per_iteration": round((t_sched + t_grow) / k * 1e6, 1)}
+        mgr.close()
+    print(json.dumps(out))
 
 
 if __name__ == "__main__":

@@ -246,3 +246,104 @@ def test_adaptive_batch_size():
     assert M.next_batch_size(128, 128, 1024, False) == 256
     assert M.next_batch_size(1024, 128, 1024, False) == 1024
     assert M.next_batch_size(512, 128, 1024, True) == 128
+
+
+def _populated(seed, num_blocks=400, n=60):
+    """A manager with RT and BE requests of random lengths, some of them with
+    checkpointed tokens (RT growth over shared BE tails)."""
+    rng = np.random.default_rng(seed)
+    m = M.BlockManager(num_blocks)
+    cls = {}
+    for rid in range(1, n + 1):
+        c = RT if rng.random() < 0.4 else BE
+        m.add(rid, c)
+        cls[rid] = c
+        try:
+            m.grow(rid, int(rng.integers(1, 90)))
+        except bros.BrosError:
+            m.release(rid)
+            del cls[rid]
+    return m, cls, rng
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_grow_batch_equals_one_call_per_request(seed):
+    # Two identical managers: one grows each request by its own restore and
+    # grow calls, the other by one batched call. Same plans (concatenated in
+    # request order), same tables, same statuses.
+    a, cls, rng = _populated(seed)
+    b, _, _ = _populated(seed)
+    ids = sorted(cls)
+    pick = [int(r) for r in rng.choice(ids, size=min(40, len(ids)), replace=False)]
+    n_new = [int(rng.integers(1, 40)) if cls[r] == RT and rng.random() < 0.3 else 1 for r in pick]
+    parts, status = [], []
+    for r, k in zip(pick, n_new):
+        got = []
+        try:
+            if a.query(r)[2]:
+                got.append(a.restore(r))
+            got.append(a.grow(r, k))
+            status.append(0)
+        except bros.BrosError as e:
+            got.append(e.plan)
+            status.append(e.status)
+        parts.append(got)
+    plan, ends, st = b.grow_batch(pick, n_new, restore_first=True)
+    assert st.tolist() == status
+    for k, field in enumerate(("victims", "move_src", "restore_pos", "written_pos")):
+        lens = [sum(len(getattr(p, field)) for p in got) for got in parts]
+        assert ends[:, k].tolist() == np.cumsum(lens).tolist(), field
+    for field in ("victims", "move_src", "move_dst", "restore_pos", "restore_dst", "written_pos", "written_slot"):
+        want = [getattr(p, field) for got in parts for p in got]
+        want = np.concatenate(want) if want else np.zeros(0)
+        assert np.array_equal(getattr(plan, field).reshape(want.shape), want), field
+    for r in ids:
+        assert np.array_equal(a.table(r), b.table(r)) and a.query(r) == b.query(r)
+    b.validate()
+
+
+def test_grow_batch_without_restore_reports_the_checkpointed_request():
+    m = M.BlockManager(1)
+    m.add(1, BE)
+    m.grow(1, 10)                     # BE tokens in slots 15..6 of the only block
+    m.add(2, RT)
+    m.grow(2, 16)                     # RT fills the block from the left: 10 BE tokens checkpointed
+    assert m.query(1)[2] > 0
+    plan, ends, st = m.grow_batch([2, 1], [1, 1], restore_first=False)
+    assert st.tolist()[1] == -7 and st.tolist()[0] in (0, -8)
+    with pytest.raises(bros.BrosError):
+        m.grow_batch([99], [1])       # unknown request: nothing changes
+
+
+def _queue(rng, ids, rt):
+    q = np.zeros(len(ids), dtype=M.SCHED_DTYPE)
+    q["id"] = ids
+    q["prefill"] = rng.random(len(ids)) < 0.3
+    q["n_new"] = np.where(q["prefill"], rng.integers(16, 200, len(ids)), 1)
+    q["ctx_after"] = rng.integers(20, 3000, len(ids))
+    if rt:
+        q["remaining_us"] = np.round(rng.uniform(50.0, 5000.0, len(ids)), 0)   # ties happen
+    else:
+        q["m_cpu"] = rng.integers(0, 30, len(ids))
+    return q
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_request_pulling_equals_the_full_sort(seed):
+    # Sec. 4.2: with the waiting queue in ascending remaining time, sorting
+    # only (the reachable part of) the pending queue and polling the two
+    # queue heads gives Alg. 1 the same RT order as sorting both together.
+    rng = np.random.default_rng(seed)
+    m, cls, _ = _populated(seed, num_blocks=3000, n=200)
+    ids = sorted(cls)
+    rt_ids = [r for r in ids if cls[r] == RT]
+    be_ids = [r for r in ids if cls[r] == BE]
+    pending = _queue(rng, rt_ids[: len(rt_ids) // 2], True)
+    waiting = _queue(rng, rt_ids[len(rt_ids) // 2:], True)
+    waiting = waiting[np.argsort(waiting["remaining_us"], kind="stable")]
+    be = _queue(rng, be_ids, False)
+    for batch in (1, 4, 16, 64, 1000):
+        for coef in (COEF, ((0.0, 0.0, 1.0), (0.0, 0.0, 1.0))):
+            full = M.schedule(m, np.concatenate([pending, waiting]), be, batch, coef)
+            pulled = M.schedule_pulled(m, pending, waiting, be, batch, coef)
+            assert pulled == full, (batch, coef)
