@@ -213,6 +213,8 @@ def main():
     ap.add_argument("--swap-slots", type=int, default=0,
                     help="also checkpoint and restore N slots per step (lazy checkpointing), the host copies "
                          "overlapping the attention")
+    ap.add_argument("--fused", action="store_true",
+                    help="run the prefill and the decode in one launch (bros_attn_mixed) instead of two calls")
     ap.add_argument("--reps", type=int, default=50,
                     help="single steps timed one by one after a cache scrub each (median, p10, p90)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
@@ -251,7 +253,7 @@ def main():
     bros.bros_check_batch(batch.block_tables, batch.dir, batch.cls, batch.ctx_lens, batch.num_blocks)
     dev = bros.to_device(batch)
     step = MixedStep(batch, dev, overlap=args.overlap, prefill_cus=args.prefill_cus, swap_slots=args.swap_slots,
-                     copy_cus=args.copy_cus, swap_serial=args.swap_serial)
+                     copy_cus=args.copy_cus, swap_serial=args.swap_serial, fused=args.fused)
     work = algorithmic_work(batch)
     stream = step.main if step.main is not None else torch.cuda.current_stream()
 
@@ -261,6 +263,7 @@ def main():
 
     K = args.steps
     side = step.side if step.overlap else stream
+    main_call = "mixed" if step.fused else "decode"   # the dominant call, bracketed in the headline pass
 
     def timed_steps(all_calls: bool):
         """K steps between two events on `stream`. The decode call is always
@@ -268,9 +271,10 @@ def main():
         all_calls every call is, for the per-call breakdown. Each event in the
         stream costs a few microseconds of the step, so the headline pass
         records only the decode's."""
-        names = ("kv_write", "prefill", "decode") + (("swap_gather", "swap_scatter") if step.swap else ())
+        names = ("kv_write",) + (("mixed",) if step.fused else ("prefill", "decode")) + \
+            (("swap_gather", "swap_scatter") if step.swap else ())
         ev = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
-              for k in (names if all_calls else ("decode",))}
+              for k in (names if all_calls else (main_call,))}
         written = [torch.cuda.Event() for _ in range(K)]
         prefilled = [torch.cuda.Event() for _ in range(K)]
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -297,8 +301,11 @@ def main():
             if step.overlap:
                 written[i].record(stream)
                 side.wait_event(written[i])
-            call("prefill", i, side, step.prefill)
-            call("decode", i, stream, step.decode)
+            if step.fused:
+                call("mixed", i, stream, step.mixed)
+            else:
+                call("prefill", i, side, step.prefill)
+                call("decode", i, stream, step.decode)
             if step.overlap:
                 prefilled[i].record(side)
                 stream.wait_event(prefilled[i])
@@ -330,8 +337,11 @@ def main():
                     a2 = torch.cuda.Event()
                     a2.record(stream)
                     side.wait_event(a2)
-                step.prefill(side)
-                step.decode(stream)
+                if step.fused:
+                    step.mixed(stream)
+                else:
+                    step.prefill(side)
+                    step.decode(stream)
                 if step.overlap:
                     b2 = torch.cuda.Event()
                     b2.record(side)
@@ -347,17 +357,23 @@ def main():
     # bracketed, then single steps with a cache scrub before each
     ms, per_head, wall_ms = timed_steps(False)
     ms_inst, per_call, _ = timed_steps(True)
-    per_call["decode_in_headline_pass"] = per_head["decode"]
+    per_call[main_call + "_in_headline_pass"] = per_head[main_call]
     reps = scrubbed_reps(max(args.reps, 1))
 
-    dec_ms = per_head.get("decode")
+    dec_ms = per_head.get(main_call)
     roof = None
     if dec_ms:
-        achieved = work["decode"]["bytes"] / (dec_ms * 1e-3) / 1e9
+        if step.fused:
+            nbytes = work["decode"]["bytes"] + work["prefill"]["bytes"]
+            kernel, traffic = "bros_attn_mixed (mixed_kernel + decode_mfma_merge_kernel)", None
+        else:
+            nbytes = work["decode"]["bytes"]
+            kernel = "bros_attn_decode (decode_mfma_kernel + decode_mfma_merge_kernel)"
+            traffic = decode_traffic(batch.name)
+        achieved = nbytes / (dec_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": decode_traffic(batch.name),
-                "kernel": "bros_attn_decode (decode_mfma_kernel + decode_mfma_merge_kernel)",
-                "bytes_per_launch": work["decode"]["bytes"], "avg_launch_us": round(dec_ms * 1e3, 2)}
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kernel,
+                "bytes_per_launch": nbytes, "avg_launch_us": round(dec_ms * 1e3, 2)}
 
     value = work["step_bytes"] / (ms * 1e-3) / 1e9
     line = {
@@ -371,7 +387,7 @@ def main():
                    "block_size": 16, "pool_blocks": batch.num_blocks, "sum_ctx": int(batch.ctx_lens.sum()),
                    "overlap": bool(step.overlap), "prefill_cus": step.prefill_cus,
                    "swap_slots": args.swap_slots, "copy_cus": step.copy_cus,
-                   "swap_serial": bool(args.swap_serial)},
+                   "swap_serial": bool(args.swap_serial), "fused": bool(step.fused)},
         "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
         "us_per_step_every_call_timed": round(ms_inst * 1e3, 2),
         "scrubbed": {"scrub": True, "scrub_bytes": SCRUB_BYTES, "reps": int(reps.size),

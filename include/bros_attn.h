@@ -200,6 +200,44 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
                             void* stream);
 
 /*
+ * bros_attn_mixed -- the prefill chunks and the decode rows of one mixed batch
+ * in one launch.
+ *
+ * Defines: the executor's batch of Sec. 6 -- prefill requests concatenated
+ * along the token axis with their shapes in a length table, decode requests
+ * after them -- computed in a single grid. The metadata rows (block_tables,
+ * dir, cls, ctx_lens) hold the prefill sequences first, rows [0,
+ * num_prefill_seqs), then the decode sequences, rows [num_prefill_seqs,
+ * num_prefill_seqs + num_decode_seqs). The results equal those of
+ *   bros_attn_prefill_chunk(out_prefill, q_prefill, cu_q, ... rows [0, P) ...)
+ *   bros_attn_decode(out_decode, q_decode, ... rows [P, P + D) ...)
+ * up to rounding (the decode's contexts may be cut between workers at other
+ * places). Each workgroup first runs one prefill unit and then takes decode
+ * tiles in proportion to the time its unit leaves it, so the prefill's
+ * uneven units no longer leave compute units idle.
+ *
+ *   out_prefill, q_prefill : [num_q_tokens][num_q_heads][head_dim]; cu_q [P + 1]
+ *   out_decode, q_decode   : [num_decode_seqs][num_q_heads][head_dim]
+ *   max_ctx_prefill, max_ctx_decode : host upper bounds of each half's contexts
+ *   workspace : at least bros_attn_workspace_size(BROS_WS_DECODE, BROS_BF16,
+ *               num_decode_seqs, num_q_heads, head_dim, max_ctx_decode) bytes,
+ *               16-byte aligned, as for bros_attn_decode.
+ * bf16 only, prefill contexts up to 32768 (BROS_E_UNSUPPORTED otherwise: use
+ * the two calls). With no prefill rows it is bros_attn_decode, with no decode
+ * rows bros_attn_prefill_chunk; when the prefill has more units than one grid
+ * holds (two workgroups per compute unit) it runs the two calls in turn.
+ * Errors as for the two calls.
+ */
+int bros_attn_mixed(void* out_prefill, const void* q_prefill, const int32_t* cu_q, int32_t num_q_tokens,
+                    int32_t max_q_len, int32_t num_prefill_seqs, int32_t max_ctx_prefill,
+                    void* out_decode, const void* q_decode, int32_t num_decode_seqs, int32_t max_ctx_decode,
+                    const void* k_pool, const void* v_pool, int32_t num_blocks,
+                    const int32_t* block_tables, int32_t max_blocks_per_seq,
+                    const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
+                    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                    float scale, int32_t dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Bytes of device workspace the call `kind` needs for `num_rows` query rows
  * (num_seqs for decode, num_q_tokens for prefill). Pure host arithmetic; it
  * does not know num_kv_heads and sizes bf16 decode for groups of up to 8

@@ -24,7 +24,7 @@ STATUS = {0: "BROS_OK", -1: "BROS_E_NULL", -2: "BROS_E_SHAPE", -3: "BROS_E_DTYPE
           -8: "BROS_E_NOMEM"}
 
 EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_write",
-            "bros_attn_decode", "bros_attn_decode_noalloc", "bros_attn_prefill_chunk", "bros_attn_workspace_size",
+            "bros_attn_decode", "bros_attn_decode_noalloc", "bros_attn_prefill_chunk", "bros_attn_mixed", "bros_attn_workspace_size",
             "bros_check_batch", "bros_stream_create_cu_share", "bros_stream_destroy",
             "bros_kv_gather", "bros_kv_scatter", "bros_check_slot_ids", "bros_copy_dma", "bros_slot_ids",
             "bros_mgr_create", "bros_mgr_destroy", "bros_mgr_add_request", "bros_mgr_release", "bros_mgr_grow",
@@ -62,6 +62,8 @@ def _load() -> ctypes.CDLL:
     lib.bros_attn_decode_noalloc.restype = ctypes.c_int
     lib.bros_attn_prefill_chunk.argtypes = [P, P, P, I, I, P, P, I, P, I, P, P, I, P, I, I, I, I, I, I, F, I, P, Z, P]
     lib.bros_attn_prefill_chunk.restype = ctypes.c_int
+    lib.bros_attn_mixed.argtypes = [P, P, P, I, I, I, I, P, P, I, I, P, P, I, P, I, P, P, I, P, I, I, I, I, F, I, P, Z, P]
+    lib.bros_attn_mixed.restype = ctypes.c_int
     lib.bros_attn_workspace_size.argtypes = [I, I, I, I, I, I]
     lib.bros_attn_workspace_size.restype = Z
     lib.bros_check_batch.argtypes = [P, I, P, P, I, P, I, I, I, I]
@@ -184,6 +186,25 @@ def bros_attn_prefill_chunk(out, q, cu_q, max_q_len: int, k_pool, v_pool, block_
                                        _dir_mode(dir, block_tables), _ptr(ctx_lens), int(max_ctx), int(ctx_lens.shape[0]), int(q.shape[1]), hkv, d, bs,
                                        float(scale), _dtype_code(q), _ptr(workspace), ws_bytes,
                                        _stream(stream)))
+
+
+def bros_attn_mixed(out_prefill, q_prefill, cu_q, max_q_len: int, max_ctx_prefill: int, out_decode, q_decode,
+                    max_ctx_decode: int, k_pool, v_pool, block_tables, dir, cls, ctx_lens, num_prefill_seqs: int,
+                    scale: float = 0.0, workspace=None, stream=None):
+    """Prefill chunks (metadata rows [0, P)) and decode rows (rows [P, S)) of
+    one concatenated batch in one launch."""
+    nb, hkv, bs, d = (int(x) for x in k_pool.shape)
+    P = int(num_prefill_seqs)
+    D = int(ctx_lens.shape[0]) - P
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    qp = q_prefill if q_prefill is not None and q_prefill.numel() else None
+    _check(LIB.bros_attn_mixed(_ptr(out_prefill) if qp is not None else None, _ptr(qp), _ptr(cu_q),
+                               0 if qp is None else int(qp.shape[0]), int(max_q_len), P, int(max_ctx_prefill),
+                               _ptr(out_decode) if D else None, _ptr(q_decode) if D else None, D, int(max_ctx_decode),
+                               _ptr(k_pool), _ptr(v_pool), nb, _ptr(block_tables), int(block_tables.shape[1]),
+                               _ptr(dir), _ptr(cls), _dir_mode(dir, block_tables), _ptr(ctx_lens),
+                               int((q_decode if D else q_prefill).shape[1]), hkv, d, bs, float(scale),
+                               _dtype_code(k_pool), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def bros_check_batch(block_tables: np.ndarray, dir, cls, ctx_lens: np.ndarray, num_blocks: int,

@@ -22,7 +22,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(HERE, "libbros_attn.so")
 
-SOURCES = ["error.cpp", "check.cpp", "api.cpp", "manager.cpp", "kv_write.hip", "decode.hip", "decode_f32.hip", "prefill.hip", "swap.hip", "noalloc.hip"]
+SOURCES = ["error.cpp", "check.cpp", "api.cpp", "manager.cpp", "kv_write.hip", "decode.hip", "decode_f32.hip", "prefill.hip", "swap.hip", "noalloc.hip", "mixed.hip"]
 ARCH = "gfx950"
 
 

@@ -235,6 +235,125 @@ int bros_attn_prefill_chunk(void* out, const void* q, const int32_t* cu_q,
   return launch_status(fn, bros::launch_decode(a, group, bf16, s));
 }
 
+int bros_attn_mixed(void* out_prefill, const void* q_prefill, const int32_t* cu_q, int32_t num_q_tokens,
+                    int32_t max_q_len, int32_t num_prefill_seqs, int32_t max_ctx_prefill,
+                    void* out_decode, const void* q_decode, int32_t num_decode_seqs, int32_t max_ctx_decode,
+                    const void* k_pool, const void* v_pool, int32_t num_blocks,
+                    const int32_t* block_tables, int32_t max_blocks_per_seq,
+                    const int8_t* dir, const uint8_t* cls, int32_t dir_per_entry, const int32_t* ctx_lens,
+                    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                    float scale, int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  const char* fn = "bros_attn_mixed";
+  int group = 0;
+  int st = check_shapes(fn, num_q_heads, num_kv_heads, head_dim, block_size, dtype, &group);
+  if (st) return st;
+  if (dtype != BROS_BF16) return fail(BROS_E_UNSUPPORTED, "%s: bf16 only (use the two calls for fp32)", fn);
+  if (num_prefill_seqs < 0 || num_decode_seqs < 0 || num_q_tokens < 0 || max_q_len < 0 || max_ctx_prefill < 0 ||
+      max_ctx_decode < 0)
+    return fail(BROS_E_SHAPE, "%s: negative count", fn);
+  if (max_ctx_prefill > bros::kPrefillMaxCtxMfma)
+    return fail(BROS_E_UNSUPPORTED, "%s: prefill context %d beyond the matrix-core path's %d (use the two calls)", fn,
+                max_ctx_prefill, bros::kPrefillMaxCtxMfma);
+  if (!ctx_lens || !block_tables) return fail(BROS_E_NULL, "%s: ctx_lens or block_tables is NULL", fn);
+  const int P = num_prefill_seqs, D = num_decode_seqs;
+  const size_t tab_off = (size_t)P * max_blocks_per_seq;
+  const int8_t* dir_d = dir ? dir + (dir_per_entry ? tab_off : (size_t)P) : nullptr;
+  const uint8_t* cls_d = cls ? cls + P : nullptr;
+  // one half only: its own call
+  if (P == 0 || num_q_tokens == 0)
+    return bros_attn_decode(out_decode, q_decode, k_pool, v_pool, num_blocks, block_tables + tab_off,
+                            max_blocks_per_seq, dir_d, cls_d, dir_per_entry, ctx_lens + P, max_ctx_decode, D,
+                            num_q_heads, num_kv_heads, head_dim, block_size, scale, dtype, workspace,
+                            workspace_bytes, stream);
+  if (D == 0)
+    return bros_attn_prefill_chunk(out_prefill, q_prefill, cu_q, num_q_tokens, max_q_len, k_pool, v_pool, num_blocks,
+                                   block_tables, max_blocks_per_seq, dir, cls, dir_per_entry, ctx_lens,
+                                   max_ctx_prefill, P, num_q_heads, num_kv_heads, head_dim, block_size, scale, dtype,
+                                   nullptr, 0, stream);
+  // both halves: validate as the two calls do
+  if (max_q_len == 0) return fail(BROS_E_SHAPE, "%s: max_q_len is 0 with %d query rows", fn, num_q_tokens);
+  if (!out_prefill || !q_prefill || !cu_q || !out_decode || !q_decode || !k_pool || !v_pool)
+    return fail(BROS_E_NULL, "%s: a tensor or offset pointer is NULL", fn);
+  st = check_meta(fn, block_tables, max_blocks_per_seq, dir, cls, dir_per_entry, num_blocks);
+  if (st) return st;
+  if (!aligned(out_prefill, 16) || !aligned(q_prefill, 16) || !aligned(out_decode, 16) || !aligned(q_decode, 16) ||
+      !aligned(k_pool, 16) || !aligned(v_pool, 16))
+    return fail(BROS_E_SHAPE, "%s: tensors must be 16-byte aligned", fn);
+  if ((long long)D * num_kv_heads * ((max_ctx_decode + 15) / 16) > 0x7fffffffLL)
+    return fail(BROS_E_SHAPE, "%s: more than 2^31 decode (row, KV head, block) tiles", fn);
+  const size_t need = bros::decode_workspace_bytes(D, num_q_heads, max_ctx_decode, true);
+  if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 16))
+    return fail(BROS_E_WORKSPACE, "%s: workspace of %zu bytes (16-byte aligned) required, got %zu at %p", fn, need,
+                workspace_bytes, workspace);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const float scale_log2 = resolve_scale(scale, head_dim);
+
+  bros::PrefillArgs pa{};
+  pa.out = out_prefill;
+  pa.q = q_prefill;
+  pa.cu_q = cu_q;
+  pa.k_pool = k_pool;
+  pa.v_pool = v_pool;
+  pa.block_tables = block_tables;
+  pa.dir = dir;
+  pa.cls = cls;
+  pa.dir_per_entry = dir_per_entry;
+  pa.ctx_lens = ctx_lens;
+  pa.num_q_tokens = num_q_tokens;
+  pa.num_seqs = P;
+  pa.num_blocks = num_blocks;
+  pa.max_blocks_per_seq = max_blocks_per_seq;
+  pa.max_ctx = max_ctx_prefill;
+  pa.num_q_heads = num_q_heads;
+  pa.num_kv_heads = num_kv_heads;
+  const int qt = bros::prefill_positions_per_tile(group);
+  pa.tiles_per_seq = (max_q_len + qt - 1) / qt;
+  pa.scale_log2 = scale_log2;
+  const long long units = (long long)P * num_kv_heads * pa.tiles_per_seq;
+
+  bros::DecodeArgs da{};
+  da.out = out_decode;
+  da.q = q_decode;
+  da.k_pool = k_pool;
+  da.v_pool = v_pool;
+  da.block_tables = block_tables + tab_off;
+  da.dir = dir_d;
+  da.cls = cls_d;
+  da.dir_per_entry = dir_per_entry;
+  da.ctx_lens = ctx_lens + P;
+  da.cu_q = nullptr;
+  da.num_rows = D;
+  da.num_seqs = D;
+  da.num_blocks = num_blocks;
+  da.max_blocks_per_seq = max_blocks_per_seq;
+  da.max_ctx = max_ctx_decode;
+  da.num_q_heads = num_q_heads;
+  da.num_kv_heads = num_kv_heads;
+  const bros::DecodePlan plan = bros::plan_decode(D, max_ctx_decode);
+  da.split_blocks = plan.split_blocks;
+  da.n_split_max = plan.n_split_max;
+  da.scale_log2 = scale_log2;
+  bros::set_decode_workspace(da, workspace, true);
+
+  // Expected costs on MI355X, fitted to a per-workgroup timeline of this
+  // launch on the mixed-step workload: a prefill unit ends at about 29 us +
+  // 0.54 us per 32-key tile (its partner on the compute unit shares the
+  // time), a decode tile takes 2.62 us on one wave. They only place work;
+  // results do not depend on them.
+  const bros::MixedModel mm{29.0f, 0.54f, 2.62f};
+  const hipError_t e = units <= 0x7fffffffLL ? bros::launch_mixed(pa, da, mm, group, (int)units, s) : hipErrorInvalidValue;
+  if (e != hipErrorInvalidValue) return launch_status(fn, e);
+  // more prefill units than one grid holds: the two calls in turn
+  st = bros_attn_prefill_chunk(out_prefill, q_prefill, cu_q, num_q_tokens, max_q_len, k_pool, v_pool, num_blocks,
+                               block_tables, max_blocks_per_seq, dir, cls, dir_per_entry, ctx_lens, max_ctx_prefill, P,
+                               num_q_heads, num_kv_heads, head_dim, block_size, scale, dtype, nullptr, 0, stream);
+  if (st) return st;
+  return bros_attn_decode(out_decode, q_decode, k_pool, v_pool, num_blocks, block_tables + tab_off,
+                          max_blocks_per_seq, dir_d, cls_d, dir_per_entry, ctx_lens + P, max_ctx_decode, D,
+                          num_q_heads, num_kv_heads, head_dim, block_size, scale, dtype, workspace, workspace_bytes,
+                          stream);
+}
+
 static int kv_move(const char* fn, bool gather, void* k_pool, void* v_pool, int32_t num_blocks,
                    const int32_t* slot_ids, int32_t num_slots, void* k_dense, void* v_dense,
                    int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t dtype, void* stream) {

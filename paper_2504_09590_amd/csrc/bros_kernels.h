@@ -47,6 +47,7 @@ struct DecodeArgs {
   float* ws_ml;           // [slots][2] (running max in log2 units, sum)
   int32_t* ws_rows;       // bf16: first tile of each row, [rows + 1]
   int32_t* ws_cut;        // bf16: per worker, the (row * Hkv + g) segment it starts and leaves cut, else -1
+  int32_t* ws_wstart;     // bf16: [0] workers W, then [1 + w] first tile of worker w (w <= W)
   int32_t num_workers;    // bf16: waves of the grid (workers beyond the tile count idle)
   int32_t num_rows;
   int32_t num_seqs;
@@ -134,6 +135,27 @@ int stream_compute_units(hipStream_t stream);
 int resident_workgroups(const void* kernel, int threads, int slot, hipStream_t stream);
 
 hipError_t launch_prefill_mfma(PrefillArgs a, int group, int num_tiles_total, hipStream_t stream);
+// The merge of the bf16 decode's cut segments (after a decode or a fused launch).
+hipError_t launch_decode_merge(const DecodeArgs& a, int group, hipStream_t stream);
+
+// Expected times that place the decode work of a fused prefill|decode launch:
+// a prefill unit costs unit_fixed_us + unit_tile_us per key tile on its
+// workgroup, a decode tile decode_tile_us on one worker (wave). Every worker
+// gets decode tiles in proportion to the time its workgroup has left after
+// its prefill unit, so that all end together.
+struct MixedModel {
+  float unit_fixed_us;
+  float unit_tile_us;
+  float decode_tile_us;
+};
+// One launch over the concatenated batch (Sec. 6): workgroup b first runs
+// prefill unit b of the matrix-core prefill (no splitting), then its waves
+// take their share of the bf16 decode tiles; then the decode merge. pa is set
+// up as for launch_prefill_mfma (its workspace fields unused), da as for
+// launch_decode with its workspace. Returns hipErrorInvalidValue when the
+// prefill units (num_units) exceed the grid or their items exceed what the
+// planner ranks; the caller then runs the two calls in turn.
+hipError_t launch_mixed(PrefillArgs pa, DecodeArgs da, MixedModel mm, int group, int num_units, hipStream_t stream);
 int prefill_positions_per_tile(int group);
 // Workspace of the matrix-core prefill (optional: without it no unit is split).
 size_t prefill_workspace_bytes();

@@ -16,6 +16,10 @@ With prefill_cus=N the two halves also get disjoint compute units: the
 prefill runs on a stream limited to the first N compute units, the write and
 the decode on a stream limited to the rest (N a multiple of 32).
 
+With fused=True the prefill and the decode run in one launch
+(bros_attn_mixed): every workgroup runs one prefill unit, then takes decode
+tiles in proportion to the time its unit left it.
+
 With swap_slots=N every step also checkpoints N slots and restores N slots
 (Sec. 5.2) through a SwapLane: the gather before the write, the scatter
 before the attention, the host copies on their own stream beside it. With
@@ -40,7 +44,7 @@ from .swap import SwapLane
 
 class MixedStep:
     def __init__(self, batch, dev: bros.DeviceBatch, overlap: bool = False, prefill_cus: int = 0,
-                 swap_slots: int = 0, copy_cus: int = 0, swap_serial: bool = False):
+                 swap_slots: int = 0, copy_cus: int = 0, swap_serial: bool = False, fused: bool = False):
         self.batch = batch
         self.dev = dev
         P, S = batch.num_prefill, batch.num_seqs
@@ -58,6 +62,9 @@ class MixedStep:
         device = dev.k_pool.device
         self.ws_decode = torch.empty(max(ws_dec, 16), dtype=torch.uint8, device=device) if ws_dec else None
         self.ws_prefill = torch.empty(max(ws_pre, 16), dtype=torch.uint8, device=device) if ws_pre else None
+        self.fused = bool(fused)
+        if self.fused and (overlap or prefill_cus):
+            raise ValueError("the fused launch runs both halves in one grid: no overlap or compute-unit split")
         self.prefill_cus = int(prefill_cus) if P > 0 and S > P else 0
         self.overlap = (overlap or self.prefill_cus > 0) and P > 0 and S > P
         self.main = None   # None: the caller's current stream
@@ -160,6 +167,13 @@ class MixedStep:
                               d.cls[P:], d.ctx_lens[P:], self.max_ctx_dec, workspace=self.ws_decode,
                               stream=stream)
 
+    def mixed(self, stream=None):
+        """Both halves in one launch (bros_attn_mixed)."""
+        d, P = self.dev, self.P
+        bros.bros_attn_mixed(self.out_prefill, d.q_prefill, d.cu_q, self.max_q_len, self.max_ctx_pre,
+                             self.out_decode, d.q_decode, self.max_ctx_dec, d.k_pool, d.v_pool, d.block_tables,
+                             d.dir, d.cls, d.ctx_lens, P, workspace=self.ws_decode, stream=stream)
+
     def run(self, write: bool = True):
         """Enqueue one whole step on the current stream (plus the side stream
         when overlapping); returns (prefill output, decode output)."""
@@ -174,7 +188,9 @@ class MixedStep:
             self.kv_write(main)
         if self.swap is not None:
             self.swap_in(main)
-        if self.overlap:
+        if self.fused:
+            self.mixed(main)
+        elif self.overlap:
             self._ev_written.record(main)
             self.side.wait_event(self._ev_written)
             self.prefill(self.side)
