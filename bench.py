@@ -163,19 +163,18 @@ def swap_figures(step, per_call, K):
     the host copies of the same rows (copy engine) timed alone, K of each."""
     import torch
     lane, n = step.swap, int(step.swap_ids.numel())
-    row = lane.out_k[0].numel() * lane.out_k.element_size()          # one slot, one tensor, all heads
-    moved = 2 * n * row                                              # K and V, each way
+    moved = 2 * lane._bytes(n)                                       # K and V, each way
     rates = {}
-    from paper_2504_09590_amd import bros
-    cs = lane.copy if lane.copy is not None else torch.cuda.current_stream()
-    for name, pairs in (("d2h", ((step.host_out_k, lane.out_k), (step.host_out_v, lane.out_v))),
-                        ("h2d", ((lane.in_k, step.host_in_k), (lane.in_v, step.host_in_v)))):
+    for name in ("d2h", "h2d"):
+        cs = (lane.out_stream if name == "d2h" else lane.in_stream) or torch.cuda.current_stream()
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(cs)
         for _ in range(K):
-            for dst, src in pairs:
-                bros.bros_copy_dma(dst, src, moved // 2, stream=cs)
+            if name == "d2h":
+                lane.copy_out(step.host_out_k, step.host_out_v, n, cs)
+            else:
+                lane.copy_in(step.host_in_k, step.host_in_v, n, cs)
         b.record(cs)
         torch.cuda.synchronize()
         us = a.elapsed_time(b) / K * 1e3
@@ -205,9 +204,6 @@ def main():
     ap.add_argument("--prefill-cus", type=int, default=0,
                     help="run the prefill on the first N compute units and the write and decode on the rest "
                          "(N a multiple of 32; implies --overlap)")
-    ap.add_argument("--copy-cus", type=int, default=0,
-                    help="with --swap-slots: run the host copies on the first N compute units and the step on the "
-                         "rest (N a multiple of 32)")
     ap.add_argument("--swap-serial", action="store_true",
                     help="with --swap-slots: enqueue the host copies on the step's stream between its kernels")
     ap.add_argument("--swap-slots", type=int, default=0,
@@ -253,7 +249,7 @@ def main():
     bros.bros_check_batch(batch.block_tables, batch.dir, batch.cls, batch.ctx_lens, batch.num_blocks)
     dev = bros.to_device(batch)
     step = MixedStep(batch, dev, overlap=args.overlap, prefill_cus=args.prefill_cus, swap_slots=args.swap_slots,
-                     copy_cus=args.copy_cus, swap_serial=args.swap_serial, fused=args.fused)
+                     swap_serial=args.swap_serial, fused=args.fused)
     work = algorithmic_work(batch)
     stream = step.main if step.main is not None else torch.cuda.current_stream()
 
@@ -386,7 +382,7 @@ def main():
                    "q_heads": batch.num_q_heads, "kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim,
                    "block_size": 16, "pool_blocks": batch.num_blocks, "sum_ctx": int(batch.ctx_lens.sum()),
                    "overlap": bool(step.overlap), "prefill_cus": step.prefill_cus,
-                   "swap_slots": args.swap_slots, "copy_cus": step.copy_cus,
+                   "swap_slots": args.swap_slots,
                    "swap_serial": bool(args.swap_serial), "fused": bool(step.fused)},
         "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
         "us_per_step_every_call_timed": round(ms_inst * 1e3, 2),

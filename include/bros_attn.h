@@ -322,22 +322,34 @@ int bros_kv_scatter(const void* k_in, const void* v_in,
                     int32_t dtype, void* stream);
 
 /*
- * bros_copy_dma -- an asynchronous copy of `bytes` bytes on a DMA engine.
+ * bros_copy_dma -- an asynchronous copy of `bytes` bytes on a copy (SDMA)
+ * engine, ordered on `stream` like a kernel launched there.
  *
  * Defines: the host copies of Sec. 5.2's lazy checkpointing, carried on their
- * own streams (Sec. 6). The copy is requested as one that needs no compute
- * unit (hipMemcpyDeviceToDeviceNoCU), so that it can proceed beside kernels
- * that occupy every compute unit. Whether a copy engine performs it is the
- * HIP runtime's choice: the ROCm 7.2 runtime uses one, while the runtime
- * bundled with PyTorch for ROCm 7.0 performs such copies as kernels
- * (__amd_rocclr_copyBuffer), which then queue behind or share compute units
- * with the attention kernels. dst and src
- * are device memory or pinned host memory (hipHostMalloc, or torch's
- * pin_memory); the ranges must not overlap. Enqueued on `stream`; returns
- * BROS_OK, BROS_E_NULL (a NULL pointer with bytes > 0) or BROS_E_HIP.
- * Copies in both directions at once share the host link badly on MI355X
- * (each falls to about a third of its rate alone), so one stream carrying
- * both directions in turn is the faster arrangement.
+ * own streams (Sec. 6), so that they proceed beside kernels that occupy every
+ * compute unit. The copy is handed to a copy engine through the ROCr runtime
+ * that the HIP runtime has loaded, not to hipMemcpyAsync (whose engine choice
+ * is the runtime's: the runtime bundled with PyTorch for ROCm 7.0 makes a copy
+ * kernel of every such copy). The engine starts once the stream's earlier
+ * work is done, and the stream's later work starts once the copy has landed:
+ * two one-lane kernels on the stream release the engine and wait for it
+ * through two HSA signals (the wait sleeps for the copy's shortest possible
+ * duration and then polls every few microseconds); no host thread waits.
+ * Host-to-device copies use one engine and device-to-host copies another, so
+ * the two directions run at once (about 57 and 48 GB/s side by side on
+ * MI355X, 56 GB/s alone).
+ *
+ * dst and src are device memory or pinned host memory (hipHostMalloc, or
+ * torch's pin_memory), not both host; the ranges must not overlap; both stay
+ * valid until the copy has ended on the stream. Copies on one engine run in
+ * the order they were requested. Not for a stream under graph capture (the
+ * engine copy would not be part of the graph). Returns BROS_OK, BROS_E_NULL
+ * (a NULL pointer with bytes > 0), BROS_E_SHAPE (pageable host memory, or
+ * both sides on the host), BROS_E_UNSUPPORTED (the stream is capturing) or
+ * BROS_E_HIP (the runtime's entry points were not found, a call failed, or an
+ * earlier copy's wait gave up after 10 s; if the stream could not take the
+ * ordering kernels, the copy has been completed before the call returned).
+ * Thread-safe.
  */
 int bros_copy_dma(void* dst, const void* src, size_t bytes, void* stream);
 

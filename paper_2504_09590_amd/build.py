@@ -22,7 +22,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(HERE, "libbros_attn.so")
 
-SOURCES = ["error.cpp", "check.cpp", "api.cpp", "manager.cpp", "kv_write.hip", "decode.hip", "decode_f32.hip", "prefill.hip", "swap.hip", "noalloc.hip", "mixed.hip"]
+SOURCES = ["error.cpp", "check.cpp", "api.cpp", "manager.cpp", "kv_write.hip", "decode.hip", "decode_f32.hip", "prefill.hip", "swap.hip", "noalloc.hip", "mixed.hip", "dma.hip"]
 ARCH = "gfx950"
 
 
@@ -66,7 +66,7 @@ def build(jobs: int = 6, verbose: bool = False) -> str:
     with ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(one, SOURCES))
     tmp = LIB_PATH + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs, "-ldl"])
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 

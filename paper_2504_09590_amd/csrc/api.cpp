@@ -393,17 +393,6 @@ int bros_kv_scatter(const void* k_in, const void* v_in,
                  const_cast<void*>(k_in), const_cast<void*>(v_in), num_kv_heads, head_dim, block_size, dtype, stream);
 }
 
-int bros_copy_dma(void* dst, const void* src, size_t bytes, void* stream) {
-  const char* fn = "bros_copy_dma";
-  if (bytes == 0) return ok();
-  if (dst == nullptr || src == nullptr) return fail(BROS_E_NULL, "%s: dst or src is NULL", fn);
-  // The no-compute-unit kind makes the runtime use a copy engine for any pair
-  // of device-addressable ranges, pinned host memory included.
-  const hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDeviceNoCU, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(BROS_E_HIP, "%s: hipMemcpyAsync of %zu bytes: %s", fn, bytes, hipGetErrorString(e));
-  return ok();
-}
-
 int bros_stream_create_cu_share(int32_t first_cu, int32_t num_cus, void** stream) {
   const char* fn = "bros_stream_create_cu_share";
   if (stream == nullptr) return fail(BROS_E_NULL, "%s: stream is NULL", fn);

@@ -22,10 +22,8 @@ tiles in proportion to the time its unit left it.
 
 With swap_slots=N every step also checkpoints N slots and restores N slots
 (Sec. 5.2) through a SwapLane: the gather before the write, the scatter
-before the attention, the host copies on their own stream beside it. With
-copy_cus=C (a multiple of 32) that copy stream runs on the first C compute
-units and the rest of the step on the others, for a runtime that performs
-host copies as kernels. With swap_serial=True the copies go on the step's own
+before the attention, the host copies on copy engines, one stream per
+direction, beside it. With swap_serial=True the copies go on the step's own
 stream between its kernels instead. The
 slots are early positions of decode sequences, which no write of the step
 touches, and the restore puts back the bytes they hold, so the step's outputs
@@ -44,7 +42,7 @@ from .swap import SwapLane
 
 class MixedStep:
     def __init__(self, batch, dev: bros.DeviceBatch, overlap: bool = False, prefill_cus: int = 0,
-                 swap_slots: int = 0, copy_cus: int = 0, swap_serial: bool = False, fused: bool = False):
+                 swap_slots: int = 0, swap_serial: bool = False, fused: bool = False):
         self.batch = batch
         self.dev = dev
         P, S = batch.num_prefill, batch.num_seqs
@@ -68,14 +66,6 @@ class MixedStep:
         self.prefill_cus = int(prefill_cus) if P > 0 and S > P else 0
         self.overlap = (overlap or self.prefill_cus > 0) and P > 0 and S > P
         self.main = None   # None: the caller's current stream
-        self.copy_cus = int(copy_cus) if swap_slots > 0 else 0
-        if self.copy_cus and self.prefill_cus:
-            raise ValueError("copy_cus and prefill_cus cannot be combined")
-        self._copy_stream = None
-        if self.copy_cus:
-            total = torch.cuda.get_device_properties(device).multi_processor_count
-            self._copy_stream = bros.bros_stream_create_cu_share(0, self.copy_cus)
-            self.main = bros.bros_stream_create_cu_share(self.copy_cus, total - self.copy_cus)
         if self.prefill_cus:
             total = torch.cuda.get_device_properties(device).multi_processor_count
             self.side = bros.bros_stream_create_cu_share(0, self.prefill_cus)
@@ -108,11 +98,13 @@ class MixedStep:
         bros.bros_check_slot_ids(ids, b.num_blocks)
         self.swap_ids = torch.from_numpy(ids).to(d.k_pool.device)
         hkv, hd = d.k_pool.shape[1], d.k_pool.shape[3]
-        self.swap = SwapLane(n, hkv, hd, d.k_pool.dtype, d.k_pool.device, copy_stream=self._copy_stream,
-                             serial=self.swap_serial)
+        self.swap = SwapLane(n, hkv, hd, d.k_pool.dtype, d.k_pool.device, serial=self.swap_serial)
         pin = dict(dtype=d.k_pool.dtype, pin_memory=True)
-        self.host_out_k, self.host_out_v = torch.empty((n, hkv, hd), **pin), torch.empty((n, hkv, hd), **pin)
-        self.host_in_k, self.host_in_v = torch.empty((n, hkv, hd), **pin), torch.empty((n, hkv, hd), **pin)
+        # K rows then V rows in one pinned buffer each way: one copy per direction
+        self.host_out = torch.empty((2 * n, hkv, hd), **pin)
+        self.host_in = torch.empty((2 * n, hkv, hd), **pin)
+        self.host_out_k, self.host_out_v = self.host_out[:n], self.host_out[n:]
+        self.host_in_k, self.host_in_v = self.host_in[:n], self.host_in[n:]
         # the rows the restore puts back: what the slots hold now
         tk = torch.empty((n, hkv, hd), dtype=d.k_pool.dtype, device=d.k_pool.device)
         tv = torch.empty_like(tk)
@@ -138,12 +130,11 @@ class MixedStep:
 
     def close(self):
         """Releases the compute-unit share streams (after their work is done)."""
-        if (self.prefill_cus or self.copy_cus) and self.main is not None:
+        if self.prefill_cus and self.main is not None:
             torch.cuda.synchronize()
-            for st in (self.side if self.prefill_cus else None, self._copy_stream, self.main):
-                if st is not None:
-                    bros.bros_stream_destroy(st)
-            self.main = self.side = self._copy_stream = None
+            for st in (self.side, self.main):
+                bros.bros_stream_destroy(st)
+            self.main = self.side = None
 
     # the three calls --------------------------------------------------------
     def kv_write(self, stream=None):

@@ -20,10 +20,10 @@ def mixed():
     return b, oracle_step(b)
 
 
-@pytest.mark.parametrize("overlap,prefill_cus,swap_slots,copy_cus",
-                         [(False, 0, 0, 0), (True, 0, 0, 0), (True, 64, 0, 0), (True, 224, 0, 0), (False, 0, 1024, 0),
-                          (True, 0, 1024, 32), (False, 0, -1024, 0)])
-def test_mixed_step_full(mixed, overlap, prefill_cus, swap_slots, copy_cus):
+@pytest.mark.parametrize("overlap,prefill_cus,swap_slots",
+                         [(False, 0, 0), (True, 0, 0), (True, 64, 0), (True, 224, 0), (False, 0, 1024),
+                          (True, 64, 1024), (False, 0, -1024)])
+def test_mixed_step_full(mixed, overlap, prefill_cus, swap_slots):
     serial = swap_slots < 0          # a negative count: the serial arrangement
     swap_slots = abs(swap_slots)
     torch = require_gpu()
@@ -32,9 +32,8 @@ def test_mixed_step_full(mixed, overlap, prefill_cus, swap_slots, copy_cus):
     b, (k1, v1, pre_ref, dec_ref) = mixed
     dev = bros.to_device(b)
     announce(f"mixed step {b.name} overlap={overlap} prefill_cus={prefill_cus} swap_slots={swap_slots} "
-             f"copy_cus={copy_cus} serial={serial}")
-    step = MixedStep(b, dev, overlap=overlap, prefill_cus=prefill_cus, swap_slots=swap_slots, copy_cus=copy_cus,
-                     swap_serial=serial)
+             f"serial={serial}")
+    step = MixedStep(b, dev, overlap=overlap, prefill_cus=prefill_cus, swap_slots=swap_slots, swap_serial=serial)
     pre, dec = step.run()
     if swap_slots:   # a second step restores what the first checkpointed
         pre, dec = step.run()

@@ -208,3 +208,91 @@ def test_copy_dma_round_trip_through_pinned_host():
     torch.cuda.synchronize()
     assert np.array_equal(host.view(torch.int16).numpy().view(np.uint16), rows)
     assert np.array_equal(_to_host(back, "bf16"), rows)
+
+
+def test_copy_dma_is_ordered_on_its_stream():
+    """Fresh data each round: a kernel writes it, the copy engine takes it to
+    pinned host memory and back into a device buffer, and a kernel on the same
+    stream reads that buffer right after. 64 MiB each way takes over a
+    millisecond on the engine, so a stream that did not wait for the copy
+    would read the previous round's values."""
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    n = 16 << 20                                              # int32 words: 64 MiB
+    s = torch.cuda.Stream()
+    host = torch.empty(n, dtype=torch.int32, pin_memory=True)
+    dev_in = torch.zeros(n, dtype=torch.int32, device="cuda")
+    src = torch.empty(n, dtype=torch.int32, device="cuda")
+    base = torch.arange(n, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    for r in range(6):
+        announce(f"bros_copy_dma ordering round {r}")
+        with torch.cuda.stream(s):
+            torch.add(base, r * 7919, out=src)                    # the kernel that writes the data
+            bros.bros_copy_dma(host, src, stream=s)
+            bros.bros_copy_dma(dev_in, host, stream=s)
+            got = dev_in.clone()                                  # the kernel that reads it
+        s.synchronize()
+        assert torch.equal(got, base + r * 7919), f"round {r}: the stream read before the copy landed"
+        assert torch.equal(host, torch.arange(n, dtype=torch.int32) + r * 7919)
+
+
+def test_copy_dma_both_directions_on_two_streams():
+    """One stream copies out while another copies in; each result matches."""
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    n = 8 << 20
+    a, b = torch.cuda.Stream(), torch.cuda.Stream()
+    src = torch.randint(-2**31, 2**31 - 1, (n,), dtype=torch.int32, device="cuda")
+    host_in = torch.randint(-2**31, 2**31 - 1, (n,), dtype=torch.int32).pin_memory()
+    host_out = torch.empty(n, dtype=torch.int32, pin_memory=True)
+    dst = torch.empty(n, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    announce("bros_copy_dma both directions at once")
+    for _ in range(3):
+        bros.bros_copy_dma(host_out, src, stream=a)
+        bros.bros_copy_dma(dst, host_in, stream=b)
+    torch.cuda.synchronize()
+    assert torch.equal(host_out, src.cpu())
+    assert torch.equal(dst.cpu(), host_in)
+
+
+def test_copy_dma_refuses_pageable_host_memory():
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    src = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    pageable = torch.zeros(1024, dtype=torch.int32)
+    host = torch.zeros(1024, dtype=torch.int32, pin_memory=True)
+    torch.cuda.synchronize()
+    assert bros.LIB.bros_copy_dma(ctypes_ptr(pageable), ctypes_ptr(src), 4096, None) == -2
+    assert bros.LIB.bros_copy_dma(ctypes_ptr(pageable), ctypes_ptr(host), 4096, None) == -2
+
+
+def ctypes_ptr(t):
+    import ctypes
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def test_copy_dma_refuses_a_capturing_stream():
+    """An engine copy is issued when requested, so it cannot be part of a
+    graph: under capture the call is refused and nothing is recorded."""
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    src = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    host = torch.zeros(1024, dtype=torch.int32, pin_memory=True)
+    out = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=s):
+        rc = bros.LIB.bros_copy_dma(ctypes_ptr(host), ctypes_ptr(src), 4096, ctypes_ptr_stream(s))
+        out.add_(1)
+    assert rc == -4
+    g.replay()
+    torch.cuda.synchronize()
+    assert int(out[0]) == 1
+
+
+def ctypes_ptr_stream(s):
+    import ctypes
+    return ctypes.c_void_p(s.cuda_stream)
