@@ -49,15 +49,16 @@ SCRUB_BYTES = 1 << 30
 # (--calibrate-copy): FETCH_SIZE reads half the bytes copied, WRITE_SIZE all of them.
 FETCH_SCALE = 2.0
 WRITE_SCALE = 1.0
-DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/csrc/decode_common.h",
+DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/csrc/decode_device.h",
+                  "paper_2504_09590_amd/csrc/decode_common.h",
                   "paper_2504_09590_amd/csrc/bros_device.h",
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 4996842.9, 16491.8),
-    "llama3-8b-decode": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 455818.3, 5174.0),
-    "llama3-8b-mixed-step": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 1131377.4, 6150.6),
-    "llama3-8b-pressure": ("73a783bf00859a60f6a11622eb8b7ac7e88613c262f35fda21e4319a680e2507", 609542.5, 10092.8),
+    "llama3-70b-decode": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 5000099.2, 19926.4),
+    "llama3-8b-decode": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 457538.1, 5694.7),
+    "llama3-8b-mixed-step": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 1132533.0, 7113.0),
+    "llama3-8b-pressure": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 606221.0, 11956.6),
 }
 
 

@@ -262,16 +262,16 @@ extern "C" int bros_copy_dma(void* dst, const void* src, size_t bytes, void* str
   const char* fn = "bros_copy_dma";
   if (bytes == 0) return ok();
   if (dst == nullptr || src == nullptr) return fail(BROS_E_NULL, "%s: dst or src is NULL", fn);
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(static_cast<hipStream_t>(stream), &cap) != hipSuccess) (void)hipGetLastError();
+  if (cap != hipStreamCaptureStatusNone)
+    return fail(BROS_E_UNSUPPORTED, "%s: the stream is being captured; an engine copy is not part of a graph", fn);
   State& s = state();
   std::lock_guard<std::mutex> lock(s.mu);
   if (!s.tried) bind_rocr(s);
   if (!s.error.empty()) return fail(BROS_E_HIP, "%s: copy engines unavailable: %s", fn, s.error.c_str());
   if (__atomic_load_n(s.timed_out, __ATOMIC_ACQUIRE) != 0)
     return fail(BROS_E_HIP, "%s: an earlier copy did not end within the wait limit; its stream went on unordered", fn);
-  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing(static_cast<hipStream_t>(stream), &cap) != hipSuccess) (void)hipGetLastError();
-  if (cap != hipStreamCaptureStatusNone)
-    return fail(BROS_E_UNSUPPORTED, "%s: the stream is being captured; an engine copy is not part of a graph", fn);
   hsa_agent_t da{0}, sa{0};
   bool dst_host = false, src_host = false;
   int st = owner(s, fn, "dst", dst, &da, &dst_host);
