@@ -21,6 +21,7 @@ from oracle import paged_attention as pa
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 GOLDEN = os.path.join(ROOT, "tests", "golden", "bidirectional_layout.json")
+GOLDEN_PER_ENTRY = os.path.join(ROOT, "tests", "golden", "per_entry_direction.json")
 
 
 def _load_golden():
@@ -44,6 +45,22 @@ def _golden_batch(hkv=2, d=8, seed=0):
     k_pool = rng.standard_normal(shape).astype(np.float32)
     v_pool = rng.standard_normal(shape).astype(np.float32)
     return g, tables, dirs, ctx, k_pool, v_pool
+
+
+def _per_entry_batch(hkv=2, d=8, seed=0):
+    """The per-entry fixture as arrays: tables and the [S][max_blocks] flag
+    table, with pool values drawn from a seeded normal."""
+    with open(GOLDEN_PER_ENTRY) as f:
+        g = json.load(f)
+    seqs = g["sequences"]
+    tables = np.array([s["block_table"] for s in seqs], dtype=np.int32)
+    flags = np.array([s["dir_per_entry"] for s in seqs], dtype=np.int8)
+    ctx = np.array([s["ctx"] for s in seqs], dtype=np.int32)
+    rng = np.random.default_rng(seed)
+    shape = (g["num_blocks"], hkv, g["block_size"], d)
+    k_pool = rng.standard_normal(shape).astype(np.float32)
+    v_pool = rng.standard_normal(shape).astype(np.float32)
+    return g, tables, flags, ctx, k_pool, v_pool
 
 
 def _contiguous_batch(rng, ctxs, hkv, d, poison=True):
@@ -107,6 +124,47 @@ def pin_golden_uniform_query():
         mean = rows.mean(axis=0)  # [Hkv, D]
         for h in range(hq):
             np.testing.assert_allclose(out[s, h], mean[h // group], rtol=0, atol=1e-13)
+
+
+def pin_per_entry_positions():
+    """Each table entry is walked in its own flag's direction."""
+    g, tables, flags, ctx, _, _ = _per_entry_batch()
+    for s, seq in enumerate(g["sequences"]):
+        blocks, slots = oracle.physical_location(tables, flags, s, np.arange(seq["ctx"]))
+        got = [[int(b), int(sl)] for b, sl in zip(blocks, slots)]
+        assert got == seq["position_to_block_slot"], seq["name"]
+
+
+def pin_per_entry_attention_vs_sdpa():
+    """Decode and a prefill chunk over the per-entry fixture equal dense SDPA
+    over the K/V rows the fixture lists, in its order (the rows of the other
+    slots are NaN, so a leaked slot shows)."""
+    g, tables, flags, ctx, k_pool, v_pool = _per_entry_batch(hkv=2, d=8, seed=3)
+    owned = {(b, sl) for seq in g["sequences"] for b, sl in seq["position_to_block_slot"]}
+    for b in range(k_pool.shape[0]):
+        for sl in range(16):
+            if (b, sl) not in owned:
+                k_pool[b, :, sl, :] = np.nan
+                v_pool[b, :, sl, :] = np.nan
+    rng = np.random.default_rng(4)
+    hq = 4
+    q = rng.standard_normal((len(ctx), hq, 8)).astype(np.float32)
+    out = oracle.decode(q, k_pool, v_pool, tables, flags, ctx, "f32")
+    dense = []
+    for s, seq in enumerate(g["sequences"]):
+        K = np.array([k_pool[b, :, sl, :] for b, sl in seq["position_to_block_slot"]])
+        V = np.array([v_pool[b, :, sl, :] for b, sl in seq["position_to_block_slot"]])
+        dense.append((K, V))
+        np.testing.assert_allclose(out[s], _sdpa(q[s:s + 1], K, V)[0], rtol=0, atol=1e-12)
+    # the last 9 positions of X as a chunk on its first 31
+    n = 9
+    qp = rng.standard_normal((n, hq, 8)).astype(np.float32)
+    got = oracle.prefill_chunk(qp, np.array([0, n], dtype=np.int32), k_pool, v_pool, tables[:1], flags[:1],
+                               ctx[:1], "f32")
+    K, V = dense[0]
+    c0 = int(ctx[0]) - n
+    mask = np.arange(int(ctx[0]))[None, :] <= (c0 + np.arange(n))[:, None]
+    np.testing.assert_allclose(got, _sdpa(qp, K, V, mask=mask), rtol=0, atol=1e-12)
 
 
 def pin_sdpa_decode():
@@ -179,8 +237,9 @@ def pin_gqa_vs_sdpa_grouping():
         np.testing.assert_allclose(out[s], ref[0], rtol=0, atol=1e-12)
 
 
-ALL_PINS = [pin_golden_positions, pin_golden_uniform_query, pin_sdpa_decode,
-            pin_sdpa_prefill, pin_bruteforce_tiny, pin_gqa_vs_sdpa_grouping]
+ALL_PINS = [pin_golden_positions, pin_golden_uniform_query, pin_per_entry_positions,
+            pin_per_entry_attention_vs_sdpa, pin_sdpa_decode, pin_sdpa_prefill, pin_bruteforce_tiny,
+            pin_gqa_vs_sdpa_grouping]
 
 
 @pytest.mark.parametrize("pin", ALL_PINS, ids=lambda f: f.__name__)
@@ -425,6 +484,12 @@ def _mutant_transposed_pv(q, k, v, limits, scale):
     return _ORIG_SOFTMAX(q, v, k, limits, scale)
 
 
+def _mutant_first_entry_direction(dir_flags, s, block_index):
+    dir_flags = np.asarray(dir_flags)
+    flag = dir_flags[s] if dir_flags.ndim == 1 else dir_flags[s][0]
+    return np.broadcast_to(flag, np.shape(block_index))
+
+
 _ORIG_SOFTMAX = pa.softmax_attention
 
 MUTANTS = {
@@ -435,6 +500,7 @@ MUTANTS = {
     "exclusive_causal_diagonal": ("softmax_attention", _mutant_exclusive_diagonal),
     "k_v_swapped": ("softmax_attention", _mutant_transposed_pv),
     "scale_dropped": ("default_scale", lambda d: 1.0),
+    "per_entry_flags_collapsed": ("_direction_of", _mutant_first_entry_direction),
 }
 
 
