@@ -16,9 +16,9 @@
 namespace bros {
 namespace {
 
-constexpr int kTokens = 8;          // tokens per workgroup
+constexpr int kTokens = 4;          // tokens per workgroup (4 measured 10 % faster than 8, 16 slower)
 constexpr int kThreads = 256;
-constexpr int kMaxIter = 8;         // 16-byte chunks per thread per pass
+constexpr int kMaxIter = 4;         // 16-byte chunks per thread per pass
 
 typedef unsigned v4u_t __attribute__((ext_vector_type(4)));   // 16 bytes (a plain vector promotes to registers)
 
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
     }                                                                                               \
   }
   BROS_KVW_STORE(0, data)
-  // Further passes (more than eight KV heads): load, then store.
+  // Further passes (more KV heads than one pass holds): load, then store.
   for (int base = kThreads * kMaxIter; base < total; base += kThreads * kMaxIter) {
     v4u_t more[kMaxIter];
 #pragma unroll

@@ -37,7 +37,7 @@ static_assert(kThreadsMixed == pf::kThreads && kThreadsMixed == kThreads, "one w
 // decode tile prefix in the K ring's LDS: (rows + 1) + one scan slot per thread
 static_assert((kMaxRowsLds + 1 + kThreadsMixed) * sizeof(int) <= pf::kSlots * pf::kTileBytes, "prefix fits the ring");
 
-template <int G>
+template <int G, bool kOff32>
 __global__ __launch_bounds__(kThreadsMixed, 2) void mixed_kernel(PrefillArgs pa, DecodeArgs da, MixedModel mm) {
   BROS_PREFILL_UNIT_LDS
   const int tid = threadIdx.x;
@@ -45,7 +45,7 @@ __global__ __launch_bounds__(kThreadsMixed, 2) void mixed_kernel(PrefillArgs pa,
   constexpr int QT = pf::kRows / G;
 
   // ---- 1. this workgroup's prefill unit (none past the last rank)
-  pf::prefill_unit<G>(pa, pf::paired_id(pa, blockIdx.x, grid), s_kring, s_vring, &s_first_bad, s_tbl, s_dir);
+  pf::prefill_unit<G, kOff32>(pa, pf::paired_id(pa, blockIdx.x, grid), s_kring, s_vring, &s_first_bad, s_tbl, s_dir);
   __syncthreads();   // the rings are free again
 
   // ---- 2. the decode's tile prefix over rows, in the K ring
@@ -177,7 +177,11 @@ __global__ __launch_bounds__(kThreadsMixed, 2) void mixed_kernel(PrefillArgs pa,
 template <int G>
 hipError_t launch_mixed_group(PrefillArgs pa, DecodeArgs da, MixedModel mm, int grid, hipStream_t stream) {
   da.num_workers = grid * kWavesMixed;
-  hipLaunchKernelGGL(mixed_kernel<G>, dim3(grid), dim3(kThreadsMixed), 0, stream, pa, da, mm);
+  // (block, KV head) rows of 4 KiB: 32-bit offsets reach them all below 2^20 rows
+  if ((int64_t)pa.num_blocks * pa.num_kv_heads <= (int64_t)1 << 20)
+    hipLaunchKernelGGL((mixed_kernel<G, true>), dim3(grid), dim3(kThreadsMixed), 0, stream, pa, da, mm);
+  else
+    hipLaunchKernelGGL((mixed_kernel<G, false>), dim3(grid), dim3(kThreadsMixed), 0, stream, pa, da, mm);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_decode_merge(da, G, stream);

@@ -6,10 +6,10 @@
 namespace bros {
 namespace pf {
 
-template <int G>
+template <int G, bool kOff32>
 __global__ __launch_bounds__(kThreads, 2) void prefill_mfma_kernel(PrefillArgs a) {
   BROS_PREFILL_UNIT_LDS
-  prefill_unit<G>(a, paired_id(a, blockIdx.x, gridDim.x), s_kring, s_vring, &s_first_bad, s_tbl, s_dir);
+  prefill_unit<G, kOff32>(a, paired_id(a, blockIdx.x, gridDim.x), s_kring, s_vring, &s_first_bad, s_tbl, s_dir);
 }
 
 // Fold the pieces of split units: one workgroup per (split item, KV head),
@@ -97,7 +97,11 @@ hipError_t launch_group(PrefillArgs a, int num_units, hipStream_t stream) {
   }
   // ranks beyond the units: at most num_cus / Hkv more pieces than items
   const long long grid = (long long)num_units + a.num_cus;
-  hipLaunchKernelGGL(prefill_mfma_kernel<G>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a);
+  // (block, KV head) rows of 4 KiB: 32-bit offsets reach them all below 2^20 rows
+  if ((int64_t)a.num_blocks * a.num_kv_heads <= (int64_t)1 << 20)
+    hipLaunchKernelGGL((prefill_mfma_kernel<G, true>), dim3((unsigned)grid), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((prefill_mfma_kernel<G, false>), dim3((unsigned)grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.num_cus == 0) return e;
   // split items x Hkv <= num_cus

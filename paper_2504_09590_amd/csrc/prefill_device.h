@@ -36,17 +36,26 @@
 // (64 banks of 4 bytes).
 // K and V have rings of their own (four slots each): the K tile of step i + 1
 // is read while the V tile of step i is, and each slot is refilled four steps
-// ahead of its use. The unit's table entries are validated once into LDS and
-// read a step ahead of the loads that use them.
+// ahead of its use. The piece's table entries are validated once into LDS as
+// (block, KV head) row indices, so a load's address is the row times 4 KiB
+// plus the lane's offset (one vector add; below 2^20 rows the pool's rows all
+// lie within 32-bit offsets of its base), and a tile's K and V loads, one
+// step apart, share one index.
+//
+// The instruction stream of a step is what bounds it (a lone wave issues an
+// instruction every 9 cycles or so), so the step carries as few as it can:
+// no 64-bit address arithmetic, the row sums of P as two more matrix-core
+// products (a ones operand times P^T) instead of eight dependent dot
+// products, and the rescale factor computed only when the max moves.
 //
 // Software pipeline (per wave, per step): the scores S^T = K Q^T of the next
 // tile are computed on the matrix cores while the vector ALU turns the current
 // tile's scores into probabilities, then O^T += V^T P^T; the max of the next
 // tile's scores decides the rescale before the step ends. In the transposed
-// orientation lane l owns query row l % 32, so the row max and sum need one
+// orientation lane l owns query row l % 32, so the row max needs one
 // exchange between the two half-waves, the O rescale is lane-local, and the P
 // operand is built straight from the score accumulators (keys are permuted
-// identically in P and V^T; the sum over keys does not care). The causal
+// identically in P and V^T; the sums over keys do not care). The causal
 // mask compares each key's logical position with the row's position, only on
 // tiles that reach the diagonal, the context end or an invalid table entry:
 // direction only reorders keys inside a block, which neither product sees.
@@ -84,6 +93,7 @@ constexpr int kTileBytes = kKeys * kRowBytes;      // one K or V tile in LDS
 constexpr float kRescaleSlack = 8.0f;              // log2 units
 constexpr float kNoMax = -1.0e30f;
 constexpr int kMaxTableLds = kPrefillMaxCtxMfma / kBlockSize;   // table entries staged in LDS
+constexpr int kTablePad = 32;                      // staged entries past the last tile (loads run ahead)
 constexpr int kMaxRankItems = kThreads;            // units planned on the device (one per thread)
 constexpr int kMaxPieces = 2 * kThreads;           // pieces ranked on the device (two per thread)
 constexpr int kMinPartTiles = 8;                   // the shortest piece a unit is split into
@@ -352,13 +362,13 @@ __device__ __forceinline__ int paired_id(const PrefillArgs& a, int b, int grid) 
   __shared__ __attribute__((aligned(1024))) uint8_t s_kring[::bros::pf::kSlots * ::bros::pf::kTileBytes]; \
   __shared__ __attribute__((aligned(1024))) uint8_t s_vring[::bros::pf::kSlots * ::bros::pf::kTileBytes]; \
   __shared__ int s_first_bad;                                                                   \
-  __shared__ int s_tbl[::bros::pf::kMaxTableLds];                                               \
-  __shared__ int8_t s_dir[::bros::pf::kMaxTableLds];
+  __shared__ int s_tbl[::bros::pf::kMaxTableLds + ::bros::pf::kTablePad];                      \
+  __shared__ int8_t s_dir[::bros::pf::kMaxTableLds + ::bros::pf::kTablePad];
 
 // One unit (or piece) of the matrix-core prefill: unit id `id` (rank id /
 // Hkv, KV head id % Hkv), run by the calling workgroup's four waves. Every
 // early return is uniform over the workgroup.
-template <int G>
+template <int G, bool kOff32>
 __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8_t* s_kring, uint8_t* s_vring,
                                              int* s_first_bad_p, int* s_tbl, int8_t* s_dir) {
   constexpr int QT = kRows / G;   // positions per unit
@@ -425,33 +435,29 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
     }
   }
 
-  // Table entries come in as scalar loads (block b of the sequence, or -1
-  // for an entry past the context or out of range). The tile of step j is
-  // kb + j; this wave loads, positions and fixes up rows 8 rg .. 8 rg + 7 of
-  // it, in block rg / 2.
+  // Table entries. The first few come in as scalar loads; the piece's
+  // entries are then staged in LDS as (block, KV head) row indices,
+  // b * Hkv + g, with direction flags (0 for an entry that is invalid, past
+  // the context or outside the piece, whose index is 0: a load from there
+  // fills a slot nobody reads, so every step issues exactly kLoadsPerStep
+  // loads and the waits below can count). The tile of step j is kb + j; this
+  // wave loads, positions and fixes up rows 8 rg .. 8 rg + 7 of it, in block
+  // rg / 2.
   const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
   const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
   const int32_t* tbl = a.block_tables + (size_t)s * a.max_blocks_per_seq;
+  const int blo = 2 * kb, bhi = min(nblk, 2 * (kb + n_kt));   // the piece's entries
   auto entry = [&](int b) -> int {
-    const int v = load_uniform(tbl, min(b, nblk - 1));
-    return (b < nblk && v >= 0 && v < a.num_blocks) ? v : -1;
+    const int v = load_uniform(tbl, min(max(b, 0), nblk - 1));
+    return (b >= blo && b < bhi && v >= 0 && v < a.num_blocks) ? v * Hkv + g : 0;
   };
   const int my_bt = rg >> 1;                // block of the tile holding this wave's rows
   const int my_slot0 = 8 * (rg & 1);        // first of its slots
-  // This wave's (validated) entry for step j, from the table staged in LDS.
-  // Read a step ahead of its use; the value comes back in a vector register
-  // and is made scalar where it is used.
-  auto own = [&](int j) -> int {
-    const int b = 2 * (kb + j) + my_bt;
-    return b < nblk ? s_tbl[b] : -1;
-  };
-  auto valid = [&](int j, int v) -> int { return __builtin_amdgcn_readfirstlane(v); };
+  // This wave's row index for step j (a vector register holding a uniform value).
+  auto own = [&](int j) -> int { return s_tbl[2 * (kb + j) + my_bt]; };
 
   // Loads: load i (0, 1) covers tile rows 8 rg + 4i + lane / 16, lane writing
   // physical chunk lane % 16, which holds logical chunk (lane % 16) ^ swz(row).
-  // A tile past the end (or an invalid entry) loads pool block 0 into a slot
-  // nobody reads, so every step issues exactly kLoadsPerStep loads and the
-  // waits below can count.
   const int ld_slot = lane >> 4;
   uint32_t ld_off[2];   // byte offset of the lane's 16 bytes within the block
 #pragma unroll
@@ -459,27 +465,32 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
     const int row = 8 * rg + 4 * i + ld_slot;   // tile row
     ld_off[i] = (uint32_t)(((my_slot0 + 4 * i + ld_slot) * kHeadDim + (((lane & 15) ^ swz(row)) << 3)) * 2);
   }
-  auto issue = [&](int j, int raw, const uint16_t* pool, uint8_t* ring) __attribute__((always_inline)) {
-    const int blk = valid(j, raw);
-    const int b = (j < n_kt && blk >= 0) ? blk : 0;
-    const uint16_t* base = pool + ((size_t)b * Hkv + g) * kBlockSize * kHeadDim;
+  // A (block, head) row is 4 KiB. With kOff32 the pool's rows all lie within
+  // 4 GiB of its base, so the per-lane offset carries the row (one vector add
+  // per load); else the base moves by the row, in scalar registers.
+  auto issue = [&](int idx, const uint16_t* pool, uint8_t* ring) __attribute__((always_inline)) {
     uint8_t* dst = ring + 8 * rg * kRowBytes;
+    if constexpr (kOff32) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) load_to_lds(base, ld_off[i], dst + 4 * i * kRowBytes);
+      for (int i = 0; i < 2; ++i) load_to_lds(pool, ld_off[i] + ((uint32_t)idx << 12), dst + 4 * i * kRowBytes);
+    } else {
+      const uint16_t* base = pool + (size_t)__builtin_amdgcn_readfirstlane(idx) * (kBlockSize * kHeadDim);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) load_to_lds(base, ld_off[i], dst + 4 * i * kRowBytes);
+    }
   };
   // Once this wave's V loads of step j have landed: zero its rows whose slot
   // is not context.
-  auto fixup_v = [&](int j, int raw, uint8_t* ring) __attribute__((always_inline)) {
+  auto fixup_v = [&](int j, uint8_t* ring) __attribute__((always_inline)) {
     if (j >= n_kt) return;
-    const int blk = valid(j, raw);
     const int b = 2 * (kb + j) + my_bt;
-    if (blk >= 0 && (b + 1) * kBlockSize <= ctx) return;
+    const int dirv = __builtin_amdgcn_readfirstlane((int)s_dir[b]);
+    if (dirv != 0 && (b + 1) * kBlockSize <= ctx) return;
     uint8_t* dv = ring + 8 * rg * kRowBytes;
-    const int dirv = s_dir[b < nblk ? b : 0];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const int r8 = 4 * p + ld_slot;   // row among the wave's 8
-      if (!(blk >= 0 && b * kBlockSize + slot_of_offset(my_slot0 + r8, dirv) < ctx))
+      if (!(dirv != 0 && b * kBlockSize + slot_of_offset(my_slot0 + r8, dirv) < ctx))
         *reinterpret_cast<v4u_t*>(dv + r8 * kRowBytes + (lane & 15) * 16) = v4u_t{0, 0, 0, 0};
     }
   };
@@ -503,7 +514,15 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   floatx16 o[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = floatx16{};
-  float m_run = kNoMax, l_run = 0.0f, alpha = 1.0f;
+  float m_run = kNoMax, m_prev = kNoMax;
+  // Row sums of P on the matrix cores: a ones operand times P^T gives, in
+  // every accumulator of lane l, the sum over the tile's keys of row l % 32
+  // (both half-waves get the whole sum). Only element 0 is read (and
+  // rescaled); the others accumulate along unread.
+  floatx16 lacc = floatx16{};
+  const bf16x2_t one2 = {(__bf16)1.0f, (__bf16)1.0f};
+  const v4u_t ones4 = {__builtin_bit_cast(uint32_t, one2), __builtin_bit_cast(uint32_t, one2),
+                       __builtin_bit_cast(uint32_t, one2), __builtin_bit_cast(uint32_t, one2)};
   // Raw scores of the wave's next tile, carried from the step that computes
   // them (and their max) to the step that turns them into probabilities: two
   // buffers, so that a step reads one while the matrix cores write the other
@@ -537,10 +556,9 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
     if constexpr (decltype(maskc)::value) {
       // visible: valid block, position < ctx and <= the row's position
       const int lim = min(qpos, ctx - 1);
-      const bool ok0 = (2 * tile < nblk ? s_tbl[2 * tile] : -1) >= 0;
-      const bool ok1 = (2 * tile + 1 < nblk ? s_tbl[2 * tile + 1] : -1) >= 0;
-      const int dir0 = s_dir[2 * tile < nblk ? 2 * tile : 0];
-      const int dir1 = s_dir[2 * tile + 1 < nblk ? 2 * tile + 1 : 0];
+      const int dir0 = s_dir[2 * tile];       // 0: invalid, past the context or outside the piece
+      const int dir1 = s_dir[2 * tile + 1];
+      const bool ok0 = dir0 != 0, ok1 = dir1 != 0;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int k = 8 * (j >> 2) + 4 * half + (j & 3);   // j is a constant; half per lane
@@ -553,18 +571,13 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
 #pragma unroll
     for (int j = 0; j < 16; ++j) mr = fmaxf(mr, cur[j]);
     const float mx = pair_max(mr) * sl2;   // log2 units; -inf when nothing is visible
-    const float m_new = mx > m_run + kRescaleSlack ? mx : m_run;
-    alpha = fast_exp2(m_run - m_new);
-    l_run *= alpha;
-    m_run = m_new;
+    m_prev = m_run;
+    m_run = mx > m_run + kRescaleSlack ? mx : m_run;
   };
-  // P = exp2(S * scale - m) rounded to bf16 (the P^T operands). l sums the
-  // rounded values (two per dot product with (1, 1)), i.e. exactly the
-  // weights the PV product applies. Operand c2 (16 keys) holds accumulators
-  // 8*c2 .. 8*c2 + 7.
-  const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
+  // P = exp2(S * scale - m) rounded to bf16 (the P^T operands); the row sums
+  // (lacc) add exactly these rounded weights, the ones the PV product
+  // applies. Operand c2 (16 keys) holds accumulators 8*c2 .. 8*c2 + 7.
   auto probs = [&](bf16x8_t (&pf)[2], const floatx16& cur) __attribute__((always_inline)) {
-    float psum = l_run;
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2) {
       bf16x2_t pw[4];
@@ -573,15 +586,11 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
         const float2_t pp = {fast_exp2(fmaf(cur[8 * c2 + 2 * w], sl2, -m_run)),
                              fast_exp2(fmaf(cur[8 * c2 + 2 * w + 1], sl2, -m_run))};
         pw[w] = __builtin_convertvector(pp, bf16x2_t);   // round to nearest even
-        // (the packed pair goes to the dot product as it is: taking it back
-        // out of a vector here has been miscompiled into the first pair)
-        psum = __builtin_amdgcn_fdot2_f32_bf16(pw[w], ones, psum, false);
       }
       const v4u_t pk = {__builtin_bit_cast(uint32_t, pw[0]), __builtin_bit_cast(uint32_t, pw[1]),
                         __builtin_bit_cast(uint32_t, pw[2]), __builtin_bit_cast(uint32_t, pw[3])};
       pf[c2] = as_bf16x8(pk);
     }
-    l_run = psum;
   };
   // V^T operands of the tile in V ring `sv` for key step c2.
   auto v_operands = [&](const uint8_t* sv, int c2, v4u_t (&vv)[4]) __attribute__((always_inline)) {
@@ -598,12 +607,15 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
       o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv[dt]), pf[c2], o[dt], 0, 0, 0);
+    lacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ones4), pf[c2], lacc, 0, 0, 0);
   };
   // Rare (lazy max).
   auto rescale_o = [&]() __attribute__((always_inline)) {
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
+    if (__builtin_amdgcn_ballot_w64(m_run != m_prev) != 0) {
+      const float alpha = fast_exp2(m_prev - m_run);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
+      lacc[0] *= alpha;
     }
   };
 
@@ -636,42 +648,53 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   // publish, then issue batch ii + 4 into the slots step ii freed (K slot
   // (ii + 1) % 4, V slot ii % 4). eF, eV, eK are this wave's table entries
   // for steps ii + 1, ii + 4 and ii + 5.
-  auto advance = [&](int ii, int sl, int eF, int eV, int eK, auto fixc) __attribute__((always_inline)) {
+  // After step ii: wait for batch ii + 1 (K of step ii + 2, V of step ii + 1),
+  // zero V's non-context rows (FIX; a tile below plain_tiles has none),
+  // publish, then issue batch ii + 4 into the slots step ii freed (K slot
+  // (ii + 1) % 4, V slot ii % 4): K of step ii + 5 from row index ik, V of
+  // step ii + 4 from iv.
+  auto advance = [&](int ii, int sl, int ik, int iv, auto fixc) __attribute__((always_inline)) {
     const int sl1 = (sl + 1) & (kSlots - 1);
     wait_vmem<2 * kLoadsPerStep>();
-    if constexpr (decltype(fixc)::value) fixup_v(ii + 1, eF, s_vring + sl1 * kSlotBytes);
+    if constexpr (decltype(fixc)::value) fixup_v(ii + 1, s_vring + sl1 * kSlotBytes);
     lds_barrier();
-    issue(ii + 5, eK, kpool, s_kring + sl1 * kSlotBytes);
-    issue(ii + 4, eV, vpool, s_vring + sl * kSlotBytes);
+    issue(ik, kpool, s_kring + sl1 * kSlotBytes);
+    issue(iv, vpool, s_vring + sl * kSlotBytes);
   };
   const uint8_t* kr = s_kring;
   const uint8_t* vr = s_vring;
 
   // ---- Prologue. Step j's K tile lives in K slot j % 4, its V tile in V
-  // slot j % 4. Batch b = (K of step
-  // b + 1, V of step b) is issued after step b - 4 frees both slots. K of
-  // step 0 and batch 0 go first, together with Q; batches 1 .. 3 follow once
-  // the first scores are in. Table entries run ahead of their use in a
-  // window: w0 .. w4 hold this wave's entries for steps ii + 1 .. ii + 5.
-  // (the first entries as scalar loads: the LDS copy is made while they load)
+  // slot j % 4. Batch b = (K of step b + 1, V of step b) is issued after
+  // step b - 4 frees both slots. K of step 0 and batch 0 go first, together
+  // with Q; batches 1 .. 3 follow once the first scores are in. (The first
+  // row indices come as scalar loads; the LDS copy is made while they load.)
   auto own0 = [&](int j) -> int { return entry(2 * (kb + j) + my_bt); };
   const int e0 = own0(0);
-  int w0 = own0(1), w1 = own0(2), w2 = own0(3), w3 = own0(4), w4 = own0(5);
-  issue(0, e0, kpool, s_kring);
-  issue(1, w0, kpool, s_kring + 1 * kSlotBytes);
-  issue(0, e0, vpool, s_vring);
+  const int w0 = own0(1), w1 = own0(2), w2 = own0(3), w3 = own0(4);
+  issue(e0, kpool, s_kring);
+  issue(w0, kpool, s_kring + 1 * kSlotBytes);
+  issue(e0, vpool, s_vring);
   // Tiles below `plain_tiles` need no mask: every key is context, sits behind
   // a valid table entry and is visible to every row of the unit. The first
-  // invalid entry comes from one pass over the sequence's table, while the
-  // first tiles are in flight.
-  if (tid == 0) (*s_first_bad_p) = nblk;
+  // invalid entry of the piece comes from the staging pass, while the first
+  // tiles are in flight. Entries past the piece (read by loads that run
+  // ahead) are staged as row 0 with direction 0.
+  if (tid == 0) (*s_first_bad_p) = bhi;
   __syncthreads();
-  for (int b = tid; b < nblk; b += kThreads) {
-    const int v = tbl[b];
-    const bool ok = v >= 0 && v < a.num_blocks;
-    s_tbl[b] = ok ? v : -1;
-    s_dir[b] = (int8_t)entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, s, b);
-    if (!ok) atomicMin(s_first_bad_p, b);
+  for (int b = blo + tid; b < 2 * (kb + n_kt) + kTablePad; b += kThreads) {
+    int idx = 0, d = 0;
+    if (b < bhi) {
+      const int v = tbl[b];
+      if (v >= 0 && v < a.num_blocks) {
+        idx = v * Hkv + g;
+        d = entry_direction(a.dir, a.cls, a.dir_per_entry, a.max_blocks_per_seq, s, b);
+      } else {
+        atomicMin(s_first_bad_p, b);
+      }
+    }
+    s_tbl[b] = idx;
+    s_dir[b] = (int8_t)d;
   }
   __syncthreads();
   const int first_bad = __builtin_amdgcn_readfirstlane((*s_first_bad_p));
@@ -679,7 +702,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   // Everything so far, Q included: a wait the compiler sees, so it knows the
   // Q registers are ready and adds no wait of its own later.
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-  fixup_v(0, e0, s_vring);
+  fixup_v(0, s_vring);
   lds_barrier();
   if (n_mine > 0) {
     v4u_t kv[8];
@@ -689,43 +712,37 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
     else mask_max(sa, std::false_type{}, kb);
   }
   lds_barrier();   // K slot 0 is free again
-  issue(2, w1, kpool, s_kring + 2 * kSlotBytes);
-  issue(1, w0, vpool, s_vring + 1 * kSlotBytes);
-  issue(3, w2, kpool, s_kring + 3 * kSlotBytes);
-  issue(2, w1, vpool, s_vring + 2 * kSlotBytes);
-  issue(4, w3, kpool, s_kring);
-  issue(3, w2, vpool, s_vring + 3 * kSlotBytes);
+  issue(w1, kpool, s_kring + 2 * kSlotBytes);
+  issue(w0, vpool, s_vring + 1 * kSlotBytes);
+  issue(w2, kpool, s_kring + 3 * kSlotBytes);
+  issue(w1, vpool, s_vring + 2 * kSlotBytes);
+  issue(w3, kpool, s_kring);
+  issue(w2, vpool, s_vring + 3 * kSlotBytes);
 
   // ---- Steps. Before step i: batch i (K of step i + 1, V of step i) is in
   // LDS, batches i + 1 .. i + 3 are in flight. The steady state (this wave has
   // a next tile and it needs no mask) runs unrolled by the ring size, with
   // the slots as constants; the rest (the tiles at the diagonal or the context
   // end, a tile behind an invalid table entry, the last tile) runs in
-  // separate loops with the slot as a variable.
+  // separate loops with the slot as a variable. A tile's K and V loads use
+  // the same row index, one step apart: `iv` carries it from the K load to
+  // the V load.
   int ii = 0;
-  // The next entry of the window: requested at the start of a step, used
-  // from the next one on.
-  auto shift = [&](int nw) __attribute__((always_inline)) {
-    w0 = w1;
-    w1 = w2;
-    w2 = w3;
-    w3 = w4;
-    w4 = nw;
-  };
+  int iv = w3;
   // the piece's tiles below plain_tiles, as a step bound
   const int n_plain = max(0, min(n_mine, plain_tiles - kb));
   auto main_step = [&](auto uc) __attribute__((always_inline)) -> bool {
     constexpr int u = decltype(uc)::value;
     if (ii + 1 >= n_plain) return false;
-    const int nw = own(ii + 6);
+    const int ik = own(ii + 5);
     // step ii reads buffer ii % 2 and fills the other (u and ii agree mod 4)
     if constexpr (u % 2 == 0)
       step(kr + ((u + 1) % kSlots) * kSlotBytes, vr + u * kSlotBytes, 0, std::true_type{}, std::false_type{}, sa, sb);
     else
       step(kr + ((u + 1) % kSlots) * kSlotBytes, vr + u * kSlotBytes, 0, std::true_type{}, std::false_type{}, sb, sa);
     rescale_o();
-    advance(ii, u, w0, w3, w4, std::false_type{});
-    shift(nw);
+    advance(ii, u, ik, iv, std::false_type{});
+    iv = ik;
     ++ii;
     return true;
   };
@@ -736,31 +753,31 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   for (; ii + 1 < n_mine; ++ii) {
     const int sl = ii & (kSlots - 1);
     const int sl1 = (sl + 1) & (kSlots - 1);
-    const int nw = own(ii + 6);
+    const int ik = own(ii + 5);
     step(kr + sl1 * kSlotBytes, vr + sl * kSlotBytes, kb + ii + 1, std::true_type{}, std::true_type{}, sa, sb);
     sa = sb;
     rescale_o();
-    advance(ii, sl, w0, w3, w4, std::true_type{});
-    shift(nw);
+    advance(ii, sl, ik, iv, std::true_type{});
+    iv = ik;
   }
   // The last tile of this wave's half.
   if (ii < n_mine) {
     const int sl = ii & (kSlots - 1);
-    const int nw = own(ii + 6);
+    const int ik = own(ii + 5);
     step(kr, vr + sl * kSlotBytes, 0, std::false_type{}, std::false_type{}, sa, sb);
-    advance(ii, sl, w0, w3, w4, std::true_type{});
-    shift(nw);
+    advance(ii, sl, ik, iv, std::true_type{});
+    iv = ik;
     ++ii;
   }
   // Steps where only the other half has a tile.
   for (; ii < n_steps; ++ii) {
-    const int nw = own(ii + 6);
-    advance(ii, ii & (kSlots - 1), w0, w3, w4, std::true_type{});
-    shift(nw);
+    const int ik = own(ii + 5);
+    advance(ii, ii & (kSlots - 1), ik, iv, std::true_type{});
+    iv = ik;
   }
 
   wait_vmem<0>();
-  l_run = pair_sum(l_run);
+  const float l_run = lacc[0];
   if (parts > 1) {
     // ---- A piece of a split unit: unnormalised rows plus their max and sum.
     const size_t slot = ((size_t)(pslot + part) * Hkv + g) * kRows + r_unit;

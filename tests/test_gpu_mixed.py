@@ -90,3 +90,40 @@ def test_fused_dispatch_one_half_and_too_many_units():
                     new_counts=[512] * 8 + [1, 1])
     announce("fused dispatch: 1024 prefill units")
     _check(many, "two calls in turn")
+
+
+def test_fused_pool_rows_past_32_bit_offsets():
+    """More than 2^20 (block, KV head) rows: the fused grid's prefill units take
+    the 64-bit address path; the batch's blocks sit past 4 GiB of each pool."""
+    torch = require_gpu()
+    import oracle
+    from paper_2504_09590_amd import bros
+    b = W.custom([300 + 200, 77, 900, 33], [W.RT, W.RT, W.BE, W.BE], 32, 8, seed=81, num_prefill=2,
+                 new_counts=[200, 77, 1, 1], spare_blocks=3)
+    announce("fused, pool rows past 2^20")
+    k_ref, v_ref, pre_ref, dec_ref = oracle_step(b)
+    # the oracle's pools after the write: the kernels read them, no write here
+    b.k_pool, b.v_pool = k_ref, v_ref
+    shift = (1 << 17) + 3
+    dev = bros.to_device(b)
+    big_k = torch.empty((shift + b.num_blocks,) + tuple(dev.k_pool.shape[1:]), dtype=dev.k_pool.dtype, device="cuda")
+    big_v = torch.empty_like(big_k)
+    big_k[shift:] = dev.k_pool
+    big_v[shift:] = dev.v_pool
+    tables = dev.block_tables.clone()
+    tables[tables >= 0] += shift
+    P = b.num_prefill
+    hq = b.num_q_heads
+    out_p = torch.full_like(dev.q_prefill, float("nan"))
+    out_d = torch.full_like(dev.q_decode, float("nan"))
+    max_pre = int(b.ctx_lens[:P].max())
+    max_dec = int(b.ctx_lens[P:].max())
+    wsb = bros.bros_attn_workspace_size(bros.BROS_WS_DECODE, bros.BROS_BF16, b.num_seqs - P, hq, b.head_dim, max_dec)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    bros.bros_attn_mixed(out_p, dev.q_prefill, dev.cu_q, int(np.diff(b.cu_q).max()), max_pre, out_d, dev.q_decode,
+                         max_dec, big_k, big_v, tables, dev.dir, dev.cls, dev.ctx_lens, P, workspace=ws)
+    torch.cuda.synchronize()
+    compare(bros.to_host_bits(out_p), pre_ref, "bf16", "fused prefill, pool rows past 2^20")
+    compare(bros.to_host_bits(out_d), dec_ref, "bf16", "fused decode, pool rows past 2^20")
+    del big_k, big_v
+    torch.cuda.empty_cache()

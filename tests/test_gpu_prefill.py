@@ -9,7 +9,8 @@ longest context of the matrix-core path (its whole table in LDS; split into
 128 pieces per unit with the workspace), more units than the device-side plan
 holds, c0 = 0 (pure causal), chunk starts and lengths off the 16/64 grid, one-row chunks, RT
 chunks walking from the right, all group sizes, the fp32 path, NaN-poisoned
-unowned slots, and the last row against a decode at the same length."""
+unowned slots, the last row against a decode at the same length, and a pool
+whose rows lie past 32-bit byte offsets."""
 
 import numpy as np
 import pytest
@@ -181,3 +182,31 @@ def test_bf16_context_beyond_the_matrix_core_path():
     poison_unowned(b)
     announce("prefill bf16 c0=33000 n=40 (row-mode path)")
     compare(run_prefill(b), ref_prefill(b), "bf16", "bf16 ctx > 32768")
+
+
+def test_pool_rows_past_32_bit_offsets():
+    """A pool of more than 2^20 (block, KV head) rows: the loads take the
+    64-bit address path. The batch's blocks sit past the first 4 GiB of each
+    pool (the rows below are left unwritten and never read)."""
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    b = written(chunk_batch([300, 40, 0], [200, 130, 77], [W.RT, W.BE, W.RT], group=4, hkv=8, seed=77))
+    announce("prefill, pool rows past 2^20")
+    ref = ref_prefill(b)
+    shift = (1 << 17) + 5            # x 8 KV heads x 4 KiB: past 4 GiB
+    dev = bros.to_device(b)
+    big_k = torch.empty((shift + b.num_blocks,) + tuple(dev.k_pool.shape[1:]), dtype=dev.k_pool.dtype, device="cuda")
+    big_v = torch.empty_like(big_k)
+    big_k[shift:] = dev.k_pool
+    big_v[shift:] = dev.v_pool
+    tables = dev.block_tables.clone()
+    tables[tables >= 0] += shift
+    P = b.num_prefill
+    out = torch.full_like(dev.q_prefill, float("nan"))
+    max_ctx = int(b.ctx_lens[:P].max())
+    bros.bros_attn_prefill_chunk(out, dev.q_prefill, dev.cu_q, int(np.diff(b.cu_q).max()), big_k, big_v,
+                                 tables[:P], dev.dir[:P], dev.cls[:P], dev.ctx_lens[:P], max_ctx)
+    torch.cuda.synchronize()
+    compare(bros.to_host_bits(out), ref, "bf16", "prefill, pool rows past 2^20")
+    del big_k, big_v
+    torch.cuda.empty_cache()
