@@ -9,8 +9,10 @@ new tokens on c0 ~ U{0..2048} cached tokens, 128 BE decode rows with ctx ~
 U{512..8192}, 32 q / 8 KV heads, head_dim 128, bf16, 40000-block pool).
 
 Timing: inputs resident in HBM; W untimed warm-up steps, then exactly K steps
-between two synchronizations, with HIP events around the decode call on the
-stream it runs on (a second pass of K steps brackets every call, for the
+between two synchronizations with HIP events only around the K steps (the
+headline pass: an event inside a step costs it a few microseconds); then a
+pass of K steps with HIP events around the decode call on the stream it runs
+on (the roofline's launch duration), and a pass that brackets every call (the
 per-call figures). Then R single steps, each after a scrub that reads and
 writes 1 GiB outside its events, give the median, p10 and p90 of a step whose
 KV comes from HBM. Prints ONE JSON line:
@@ -260,18 +262,19 @@ def main():
 
     K = args.steps
     side = step.side if step.overlap else stream
-    main_call = "mixed" if step.fused else "decode"   # the dominant call, bracketed in the headline pass
+    main_call = "mixed" if step.fused else "decode"   # the dominant call, bracketed for the roofline
 
-    def timed_steps(all_calls: bool):
-        """K steps between two events on `stream`. The decode call is always
-        bracketed by events of its own (the roofline's launch duration); with
-        all_calls every call is, for the per-call breakdown. Each event in the
-        stream costs a few microseconds of the step, so the headline pass
-        records only the decode's."""
+    def timed_steps(bracket: str):
+        """K steps between two events on `stream`. bracket "none": no other
+        event (the headline pass; each event in the stream costs a step a few
+        microseconds); "main": the dominant call bracketed by events of its own
+        (the roofline's launch duration); "all": every call, for the per-call
+        breakdown."""
         names = ("kv_write",) + (("mixed",) if step.fused else ("prefill", "decode")) + \
             (("swap_gather", "swap_scatter") if step.swap else ())
+        chosen = {"none": (), "main": (main_call,), "all": names}[bracket]
         ev = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
-              for k in (names if all_calls else (main_call,))}
+              for k in chosen}
         written = [torch.cuda.Event() for _ in range(K)]
         prefilled = [torch.cuda.Event() for _ in range(K)]
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -284,7 +287,7 @@ def main():
                 fn(s)
 
         if step.swap:
-            step.swap.timing = [] if all_calls else None
+            step.swap.timing = [] if bracket == "all" else None
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         start.record(stream)
@@ -350,14 +353,16 @@ def main():
         del scrub
         return np.array([a.elapsed_time(b) for a, b in ev])
 
-    # the headline pass (decode events only), then a pass with every call
-    # bracketed, then single steps with a cache scrub before each
-    ms, per_head, wall_ms = timed_steps(False)
-    ms_inst, per_call, _ = timed_steps(True)
-    per_call[main_call + "_in_headline_pass"] = per_head[main_call]
+    # the headline pass (no event inside a step), a pass with the dominant
+    # call bracketed, a pass with every call bracketed, then single steps with
+    # a cache scrub before each
+    ms, _, wall_ms = timed_steps("none")
+    ms_main, per_main, _ = timed_steps("main")
+    ms_inst, per_call, _ = timed_steps("all")
+    per_call[main_call + "_alone_bracketed"] = per_main[main_call]
     reps = scrubbed_reps(max(args.reps, 1))
 
-    dec_ms = per_head.get(main_call)
+    dec_ms = per_main.get(main_call)
     roof = None
     if dec_ms:
         if step.fused:
@@ -386,6 +391,7 @@ def main():
                    "swap_slots": args.swap_slots,
                    "swap_serial": bool(args.swap_serial), "fused": bool(step.fused)},
         "per_call_us": {k: round(v * 1e3, 2) for k, v in per_call.items()},
+        "us_per_step_main_call_timed": round(ms_main * 1e3, 2),
         "us_per_step_every_call_timed": round(ms_inst * 1e3, 2),
         "scrubbed": {"scrub": True, "scrub_bytes": SCRUB_BYTES, "reps": int(reps.size),
                      "us_p10": round(float(np.percentile(reps, 10)) * 1e3, 2),
