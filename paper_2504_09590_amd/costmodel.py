@@ -18,16 +18,21 @@ coincide; for a batch the paper's Ln * La counts cross-request pairs that no
 kernel computes. Both fits are reported.
 
     python -m paper_2504_09590_amd.costmodel           # profile on the GPU, fit, print JSON
+    python -m paper_2504_09590_amd.costmodel --out paper_2504_09590_amd/costmodel_mi355x.json
 
 The profiler builds its batches directly on the device (random bf16 values,
 tables from a random permutation of one pool), times each call with HIP
-events, and takes the median of its repetitions.
+events, and takes the median of its repetitions. costmodel_mi355x.json, next
+to this module, holds the model fitted this way on one MI355X; the block
+manager's benchmark (manager.main) prices its batches with it.
 """
+
 
 from __future__ import annotations
 
 import argparse
 import json
+import os
 import sys
 from dataclasses import dataclass, field
 
@@ -57,24 +62,33 @@ def features(form: str, ln, la, pairs) -> np.ndarray:
     return np.stack([ln, inter, np.ones_like(ln)], axis=-1)
 
 
+def _nonneg_lstsq(A: np.ndarray, y: np.ndarray) -> np.ndarray:
+    """argmin |A x - y| over x >= 0: every term of the model is a cost (per
+    token, per attended pair, per launch), so none may be negative. The
+    columns are scaled to unit norm first (they span many decades)."""
+    from scipy.optimize import nnls
+    norm = np.linalg.norm(A, axis=0)
+    norm[norm == 0] = 1.0
+    x, _ = nnls(A / norm, y)
+    return x / norm
+
+
 def fit(samples, form: str) -> np.ndarray:
-    """(a0, a1, b) minimising the squared RELATIVE error over the samples (a
-    profile spans several decades of time; plain least squares would fit only
-    the largest points)."""
+    """(a0, a1, b) >= 0 minimising the squared RELATIVE error over the samples
+    (a profile spans several decades of time; plain least squares would fit
+    only the largest points)."""
     X = features(form, [s.ln for s in samples], [s.la for s in samples], [s.pairs for s in samples])
     t = np.array([s.t_us for s in samples], dtype=np.float64)
     w = 1.0 / t
-    coef, *_ = np.linalg.lstsq(X * w[:, None], t * w, rcond=None)
-    return coef
+    return _nonneg_lstsq(X * w[:, None], t * w)
 
 
 def fit_swap(sizes_bytes, t_us) -> np.ndarray:
-    """(seconds per byte expressed as us/B, fixed us) of a linear swap-time model."""
+    """(seconds per byte expressed as us/B, fixed us) >= 0 of a linear swap-time model."""
     X = np.stack([np.asarray(sizes_bytes, dtype=np.float64), np.ones(len(sizes_bytes))], axis=-1)
     t = np.asarray(t_us, dtype=np.float64)
     w = 1.0 / t
-    coef, *_ = np.linalg.lstsq(X * w[:, None], t * w, rcond=None)
-    return coef
+    return _nonneg_lstsq(X * w[:, None], t * w)
 
 
 @dataclass
@@ -114,6 +128,15 @@ class CostModel:
     def from_json(text: str) -> "CostModel":
         d = json.loads(text)
         return CostModel(coef=d["coef"], swap=d["swap"])
+
+
+MODEL_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "costmodel_mi355x.json")
+
+
+def load_fitted(path: str = MODEL_PATH) -> CostModel:
+    """The model fitted on one MI355X (written by main with --out)."""
+    with open(path) as f:
+        return CostModel.from_json(f.read())
 
 
 def power_grid(lo: int, hi: int) -> list[int]:
@@ -220,6 +243,7 @@ def profile_swap(torch, bros, sizes_bytes, reps=7):
 def main(argv=None):
     ap = argparse.ArgumentParser(description="profile this library's kernels and fit the Sec. 4.1 cost model")
     ap.add_argument("--reps", type=int, default=7)
+    ap.add_argument("--out", default=None, help="also write the fitted model (CostModel JSON) to this file")
     args = ap.parse_args(argv)
     import torch
     from . import bros
@@ -255,6 +279,9 @@ def main(argv=None):
                                         "GB/s": float(1e-3 / model.swap[key][0]),
                                         "max_rel_err": float(np.max(np.abs(pred - sw[key]) / np.array(sw[key])))}
     report["model"] = json.loads(model.to_json())
+    if args.out:
+        with open(args.out, "w") as f:
+            f.write(model.to_json() + "\n")
     print(json.dumps(report), flush=True)
 
 

@@ -51,8 +51,14 @@ struct Block {
   int32_t rt_e = 0, be_e = 0;   // the owners' table entries mapped here
   int32_t rt_n = 0, be_n = 0;   // their tokens present in the block
   bool preempted = false;
+  // Which block list holds the block (at most one: free, RT-open or BE-open)
+  // and under which count of empty slots, so that a list update touches only
+  // the list the block is in.
+  int8_t listed = 0;   // kListedRt | kListedBe | kListedFree
+  int8_t key = 0;
   int empty() const { return kBS - rt_n - be_n; }
 };
+constexpr int8_t kListedRt = 1, kListedBe = 2, kListedFree = 4;
 
 struct Request {
   int32_t cls = BROS_RT;
@@ -82,7 +88,10 @@ struct Plan {
 class Manager {
  public:
   explicit Manager(int32_t n) : blocks_(n) {
-    for (int32_t b = 0; b < n; ++b) free_.insert(b);
+    for (int32_t b = 0; b < n; ++b) {
+      free_.insert(b);
+      blocks_[b].listed = kListedFree;
+    }
   }
 
   int32_t num_blocks() const { return (int32_t)blocks_.size(); }
@@ -278,6 +287,7 @@ class Manager {
     if (!free_.empty()) {
       const int32_t b = *free_.begin();
       free_.erase(free_.begin());
+      blocks_[b].listed = 0;
       return b;
     }
     OpenSet& open = cls == BROS_RT ? rt_open_ : be_open_;
@@ -286,6 +296,7 @@ class Manager {
       if (it->second == exclude) continue;
       const int32_t b = it->second;
       open.erase(it);
+      blocks_[b].listed = 0;
       return b;
     }
     return -1;
@@ -329,22 +340,29 @@ class Manager {
   }
 
   void unlist(int32_t b) {
-    const Block& blk = blocks_[b];
-    rt_open_.erase({-blk.empty(), b});
-    be_open_.erase({-blk.empty(), b});
-    free_.erase(b);
+    Block& bl = blocks_[b];
+    if (bl.listed & kListedRt) rt_open_.erase({-bl.key, b});
+    if (bl.listed & kListedBe) be_open_.erase({-bl.key, b});
+    if (bl.listed & kListedFree) free_.erase(b);
+    bl.listed = 0;
   }
 
   void refresh(int32_t b) {
     const Block& blk = blocks_[b];
-    rt_open_.erase({-blk.empty(), b});
-    be_open_.erase({-blk.empty(), b});
-    if (blk.rt < 0 && blk.be < 0) {
+    const int8_t want = (blk.rt < 0 && blk.be < 0) ? kListedFree
+                        : (blk.rt < 0 ? kListedRt : 0) | (blk.be < 0 ? kListedBe : 0);
+    const int8_t key = (int8_t)blk.empty();
+    if (blk.listed == want && (want == 0 || want == kListedFree || blk.key == key)) return;   // already so
+    unlist(b);
+    Block& bl = blocks_[b];
+    bl.listed = want;
+    bl.key = key;
+    if (want == kListedFree) {
       free_.insert(b);
       return;
     }
-    if (blk.rt < 0) rt_open_.insert({-blk.empty(), b});
-    if (blk.be < 0) be_open_.insert({-blk.empty(), b});
+    if (want & kListedRt) rt_open_.insert({-key, b});
+    if (want & kListedBe) be_open_.insert({-key, b});
   }
 
   std::vector<Block> blocks_;

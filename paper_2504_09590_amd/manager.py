@@ -278,7 +278,9 @@ def main(argv=None):
     ap.add_argument("--batch", type=int, default=256)
     ap.add_argument("--seed", type=int, default=0)
     args = ap.parse_args(argv)
-    coef = ((7.3e-3, 1.0e-5, 18.4), (8.8e-3, 6.5e-4, 23.7))   # the fitted per-request form (us)
+    from .costmodel import load_fitted
+    fitted = load_fitted()   # the per-request form fitted on this library's kernels (us)
+    coef = (tuple(fitted.coef["prefill/per_request"]), tuple(fitted.coef["decode/per_request"]))
     out = {"requests": args.requests, "blocks": args.blocks, "batch": args.batch, "iterations": args.iterations}
     for mode in ("per_request", "batched"):
         rng = np.random.default_rng(args.seed)

@@ -65,3 +65,21 @@ def test_json_round_trip():
     m2 = cm.CostModel.from_json(m.to_json())
     assert m2.coef == m.coef and m2.swap == m.swap
     assert float(m2.predict("decode", 10, 20)) == pytest.approx(1 * 10 + 2 * 200 + 3)
+
+
+def test_fit_keeps_every_term_non_negative():
+    # a decode profile whose time barely grows with the batch: an unconstrained
+    # fit gives the per-request term a small negative value, the fit clamps it
+    grid = [(b, c) for b in cm.power_grid(8, 256) for c in cm.power_grid(256, 8192)]
+    s = []
+    for b, c in grid:
+        t = 22.0 + 6.0e-4 * b * c - 0.002 * b
+        s.append(cm.Sample("decode", b, b * c, b * c, t, b))
+    free, *_ = np.linalg.lstsq(cm.features("per_request", [x.ln for x in s], [x.la for x in s],
+                                           [x.pairs for x in s]) / np.array([x.t_us for x in s])[:, None],
+                               np.ones(len(s)), rcond=None)
+    assert free[0] < 0
+    coef = cm.fit(s, "per_request")
+    assert np.all(coef >= 0) and coef[0] == 0.0
+    model = cm.CostModel(coef={"decode/per_request": coef})
+    assert cm.relative_errors(model, s, "per_request").max() < 0.02
