@@ -46,7 +46,8 @@ struct DecodeArgs {
   float* ws_acc;          // [slots][D] unnormalised partial outputs
   float* ws_ml;           // [slots][2] (running max in log2 units, sum)
   int32_t* ws_rows;       // bf16: first tile of each row, [rows + 1]
-  int32_t* ws_cut;        // bf16: per worker, the (row * Hkv + g) segment it starts and leaves cut, else -1
+  int32_t* ws_cut;        // bf16: per worker, [2 w] the (row * Hkv + g) segment it starts and leaves cut, else -1;
+                          // [2 w + 1] the worker holding that segment's last tile, or -1 if not computed
   int32_t* ws_wstart;     // bf16: [0] workers W, then [1 + w] first tile of worker w (w <= W)
   int32_t num_workers;    // bf16: waves of the grid (workers beyond the tile count idle)
   int32_t num_rows;

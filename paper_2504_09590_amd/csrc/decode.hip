@@ -27,17 +27,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       a.ws_wstart[1 + w] = (int)((int64_t)w * total / max(workers, 1));
   }
   const int wid = blockIdx.x * kWaves + wave_id_uniform();
-  if (wid >= workers) return;
+  if (wid >= workers) {
+    if (wid < a.num_workers && (threadIdx.x & (kWave - 1)) == 0) a.ws_cut[2 * wid] = -1;   // idle: nothing to merge
+    return;
+  }
   const int t0 = (int)((int64_t)wid * total / workers);
   const int t1 = (int)((int64_t)(wid + 1) * total / workers);
-  decode_worker<G>(a, s_pre, chunk, nch, wid, t0, t1 - t0);
+  decode_worker<G>(a, s_pre, chunk, nch, wid, t0, t1 - t0, total, workers);
 }
 
 // Segments cut between workers: o = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w -
 // M) l_w over the partials of workers w0 .. w1. The decode kernel's worker
 // w0 (the one that started the segment and left it unfinished) named the
-// segment in its entry of the cut list; every other entry is -1, so the merge
-// grid has one wave per worker and most waves return after one load. Segments
+// segment in its entry of the cut list, with w1 when its shares are the even
+// split (then every worker has tiles and the merge reads nothing else before
+// the partials); every other entry is -1, so the merge grid has one wave per
+// worker and most waves return after one load. Segments
 // a single worker covered were written directly, and rows without context
 // were written as zeros by that worker (a worker that sees no tile of a row
 // never runs for it: rows without context have no tiles, so they are written
@@ -63,35 +68,40 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void decode_mfma_merge_kernel(
       for (int i = lane; i < a.num_q_heads * kHeadDim / 2; i += kWave) z[i] = 0u;
     }
   }
-  // the decode grid's partition of the tiles: workers W, worker w's tiles
-  // start at starts[w] (starts[W] = all tiles); a worker may have none
-  const int workers = a.ws_wstart[0];
-  const int32_t* starts = a.ws_wstart + 1;
-  if (item >= workers) return;
-  const int code = a.ws_cut[item];
+  // every worker of the grid wrote its cut-list entry (idle ones -1)
+  if (item >= a.num_workers) return;
+  const int code = a.ws_cut[2 * item];
   if (code < 0) return;
   const int nkv = a.num_kv_heads;
   const int row = __builtin_amdgcn_readfirstlane(code / nkv);
   const int g = __builtin_amdgcn_readfirstlane(code - (code / nkv) * nkv);
-  int s, ctx;
-  resolve_row(a, row, s, ctx);
-  const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
-  const int64_t first_tile = (int64_t)a.ws_rows[row] + (int64_t)g * nblk;
   const int w0 = item;
-  // w1: the worker holding the segment's last tile (the last worker whose
-  // share starts at or before it), found 64 workers per step
-  const int64_t last_tile = first_tile + nblk - 1;
-  int w1 = w0;
-  for (int base = w0 + 1; base < workers; base += kWave) {
-    const int w = base + lane;
-    const bool before = w < workers && starts[w] <= last_tile;
-    const uint64_t m = __builtin_amdgcn_ballot_w64(before);
-    w1 = base + __builtin_popcountll(m) - 1;
-    if (m != ~0ull) break;
+  int w1 = __builtin_amdgcn_readfirstlane(a.ws_cut[2 * item + 1]);
+  // the decode grid's partition of the tiles: workers W, worker w's tiles
+  // start at starts[w] (starts[W] = all tiles); a worker may have none, but
+  // not under the even split (w1 given)
+  const int32_t* starts = a.ws_wstart + 1;
+  const bool even = w1 >= 0;
+  if (!even) {
+    // w1: the worker holding the segment's last tile (the last worker whose
+    // share starts at or before it), found 64 workers per step
+    const int workers = a.ws_wstart[0];
+    int s, ctx;
+    resolve_row(a, row, s, ctx);
+    const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
+    const int64_t last_tile = (int64_t)a.ws_rows[row] + (int64_t)g * nblk + nblk - 1;
+    w1 = w0;
+    for (int base = w0 + 1; base < workers; base += kWave) {
+      const int w = base + lane;
+      const bool before = w < workers && starts[w] <= last_tile;
+      const uint64_t m = __builtin_amdgcn_ballot_w64(before);
+      w1 = base + __builtin_popcountll(m) - 1;
+      if (m != ~0ull) break;
+    }
+    w1 = __builtin_amdgcn_readfirstlane(max(w1, w0));
   }
-  w1 = __builtin_amdgcn_readfirstlane(max(w1, w0));
   // a worker with no tiles wrote no partial
-  auto has_tiles = [&](int w) -> bool { return starts[w + 1] > starts[w]; };
+  auto has_tiles = [&](int w) -> bool { return even || starts[w + 1] > starts[w]; };
   const int hl = lane / L, sub = lane % L;
   const size_t seg = (size_t)row * nkv + g;
   // the head's max over the partials (lanes of the head take every L-th one)
@@ -254,7 +264,7 @@ size_t decode_workspace_bytes(int32_t num_rows, int32_t num_q_heads, int32_t max
     const int gmax = num_q_heads < 8 ? num_q_heads : 8;
     const size_t slots = (size_t)num_rows * num_q_heads + (size_t)kWaves * kMaxDecodeGrid * gmax;
     return round_up_256(((size_t)num_rows + 1) * sizeof(int32_t)) + round_up_256(slots * kHeadDim * sizeof(float)) +
-           round_up_256(slots * 2 * sizeof(float)) + round_up_256((size_t)kWaves * kMaxDecodeGrid * sizeof(int32_t)) +
+           round_up_256(slots * 2 * sizeof(float)) + round_up_256((size_t)2 * kWaves * kMaxDecodeGrid * sizeof(int32_t)) +
            round_up_256(((size_t)kWaves * kMaxDecodeGrid + 2) * sizeof(int32_t));
   }
   const DecodePlan p = plan_decode(num_rows, max_ctx);
@@ -273,7 +283,7 @@ void set_decode_workspace(DecodeArgs& a, void* ws, bool bf16) {
     a.ws_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(a.ws_acc) + round_up_256(slots * kHeadDim * sizeof(float)));
     a.ws_cut = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(a.ws_ml) + round_up_256(slots * 2 * sizeof(float)));
     a.ws_wstart = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(a.ws_cut) +
-                                             round_up_256((size_t)kWaves * kMaxDecodeGrid * sizeof(int32_t)));
+                                             round_up_256((size_t)2 * kWaves * kMaxDecodeGrid * sizeof(int32_t)));
     return;
   }
   a.ws_rows = nullptr;

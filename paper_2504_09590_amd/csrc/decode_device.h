@@ -178,9 +178,12 @@ static __device__ void locate(const DecodeArgs& a, const int* s_pre, int chunk, 
 // One worker's share: tiles [t0, t0 + n) of the (row, KV head, block) order
 // (n >= 1), the tile prefix over rows in LDS (s_pre, chunk, nch) as
 // build_tile_prefix left it. Run by one wave; `wid` names its partial slots.
+// With `workers` > 0 the shares are the even split of `total` tiles over
+// `workers` workers, so the worker holding any tile is known in closed form;
+// 0 leaves that to the merge.
 template <int G>
 __device__ __forceinline__ void decode_worker(const DecodeArgs& a, const int* s_pre, int chunk, int nch, int wid,
-                                              int t0, int n) {
+                                              int t0, int n, int total, int workers) {
   static_assert(G >= 1 && G <= 16, "heads of a group must fit the 16 MFMA columns");
   const int lane = threadIdx.x & (kWave - 1);
   const int grp = lane >> 4;
@@ -289,9 +292,19 @@ __device__ __forceinline__ void decode_worker(const DecodeArgs& a, const int* s_
     const bool seg_end = c0.b == c0.nblk - 1 || i + 1 == n;
     if (i + 1 == n) {
       // this worker's entry of the cut list: the segment it started and
-      // leaves unfinished (the merge folds it), else -1
+      // leaves unfinished (the merge folds it), else -1; and the worker that
+      // holds the segment's last tile, the largest w with
+      // floor(w total / workers) <= that tile (-1: the merge finds it)
       const bool starts_cut = whole && c0.b != c0.nblk - 1;
-      if (lane == 0) a.ws_cut[wid] = starts_cut ? c0.row * nkv + c0.g : -1;
+      int w1 = -1;
+      if (starts_cut && workers > 0) {
+        const int64_t last = (int64_t)t0 + i + (c0.nblk - 1 - c0.b);
+        w1 = (int)(((last + 1) * workers - 1) / total);
+      }
+      if (lane == 0) {
+        a.ws_cut[2 * wid] = starts_cut ? c0.row * nkv + c0.g : -1;
+        a.ws_cut[2 * wid + 1] = w1;
+      }
     }
     // K and query registers are free: keys kDepth tiles ahead (and the query
     // of the next tile's segment)

@@ -168,10 +168,10 @@ __global__ __launch_bounds__(kThreadsMixed, 2) void mixed_kernel(PrefillArgs pa,
   const int t0 = __builtin_amdgcn_readfirstlane(first_tile(blockIdx.x, wave));
   const int t1 = __builtin_amdgcn_readfirstlane(first_tile(blockIdx.x, wave + 1));   // k = 4: s_off[b + 1]
   if (t1 <= t0) {
-    if ((tid & (kWave - 1)) == 0) da.ws_cut[wid] = -1;   // no tiles: nothing for the merge
+    if ((tid & (kWave - 1)) == 0) da.ws_cut[2 * wid] = -1;   // no tiles: nothing for the merge
     return;
   }
-  dm::decode_worker<G>(da, s_pre, chunk, nch, wid, t0, t1 - t0);
+  dm::decode_worker<G>(da, s_pre, chunk, nch, wid, t0, t1 - t0, 0, 0);   // (uneven shares: the merge finds the last worker)
 }
 
 template <int G>
