@@ -22,6 +22,17 @@ constexpr int kMaxIter = 4;         // 16-byte chunks per thread per pass
 
 typedef unsigned v4u_t __attribute__((ext_vector_type(4)));   // 16 bytes (a plain vector promotes to registers)
 
+// n / d for 0 <= n < 2^22 and d >= 1, with rcp = 1 / d: the float estimate is
+// within one of the quotient, and one correction step makes it exact (a few
+// instructions instead of the long integer division sequence).
+__device__ __forceinline__ int div_small(int n, int d, float rcp) {
+  int q = (int)((float)n * rcp);
+  const int r = n - q * d;
+  q += (r >= d) ? 1 : 0;
+  q -= (r < 0) ? 1 : 0;
+  return q;
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
   __shared__ int s_seq[kTokens];   // the sequence holding each token, or -1
@@ -35,30 +46,45 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
   constexpr int kChunksPerRow = kHeadDim * kElem / 16;     // 16-byte chunks per head row
   const int chunks_per_token = a.num_kv_heads * kChunksPerRow;   // per tensor
   const int total = kTokens * 2 * chunks_per_token;
+  const float rcp_cpt = 1.0f / (float)chunks_per_token;
   const uint8_t* __restrict__ knew = static_cast<const uint8_t*>(a.k_new);
   const uint8_t* __restrict__ vnew = static_cast<const uint8_t*>(a.v_new);
   uint8_t* __restrict__ kpool = static_cast<uint8_t*>(a.k_pool);
   uint8_t* __restrict__ vpool = static_cast<uint8_t*>(a.v_pool);
-  const size_t row_bytes = (size_t)kHeadDim * kElem;
+  constexpr uint32_t kRowBytes = kHeadDim * kElem;
+  const int n_tok = min(kTokens, a.num_new_tokens - t0);   // tokens of this workgroup (>= 1)
 
-  // Chunk idx of the workgroup: token, tensor (0 = K, 1 = V), chunk within the token.
-#define BROS_KVW_SPLIT(idx)                                  \
-  const int tok = (idx) / (2 * chunks_per_token);            \
-  const int rem = (idx) - tok * 2 * chunks_per_token;        \
-  const int tensor = rem / chunks_per_token;                 \
-  const int c = rem - tensor * chunks_per_token;
+  // Chunk idx of the workgroup: (token, tensor) pair tt = idx / chunks_per_token
+  // (token tt / 2, tensor tt % 2: 0 = K, 1 = V), chunk c within the token's
+  // rows. `part` is its offset inside a block's rows for that KV head:
+  // (h * 16 slots) rows plus the chunk within the row.
+  struct Chunk {
+    int tok, tensor, c;
+    uint32_t part;
+    bool live;
+  };
+  auto split = [&](int idx) -> Chunk {
+    Chunk k;
+    const int tt = div_small(idx, chunks_per_token, rcp_cpt);
+    k.c = idx - tt * chunks_per_token;
+    k.tok = tt >> 1;
+    k.tensor = tt & 1;
+    const int h = k.c / kChunksPerRow, cc = k.c % kChunksPerRow;   // (constant divisor: a shift)
+    k.part = ((uint32_t)h * kBlockSize) * kRowBytes + (uint32_t)cc * 16;
+    k.live = idx < total && k.tok < n_tok;
+    return k;
+  };
 
   // Source rows of the first pass: they do not depend on where the tokens go,
   // so they are requested before the destinations are resolved.
   v4u_t data[kMaxIter];
+  Chunk ch[kMaxIter];
 #pragma unroll
   for (int it = 0; it < kMaxIter; ++it) {
-    const int idx = it * kThreads + tid;
-    if (idx < total) {
-      BROS_KVW_SPLIT(idx)
-      if (t0 + tok < a.num_new_tokens)
-        data[it] = *reinterpret_cast<const v4u_t*>((tensor ? vnew : knew) + ((size_t)(t0 + tok) * chunks_per_token + c) * 16);
-    }
+    ch[it] = split(it * kThreads + tid);
+    if (ch[it].live)
+      data[it] = *reinterpret_cast<const v4u_t*>((ch[it].tensor ? vnew : knew) +
+                                                   ((size_t)(t0 + ch[it].tok) * chunks_per_token + ch[it].c) * 16);
   }
 
   // Destinations, in two rounds of loads. First, thread j checks whether
@@ -72,7 +98,7 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
   for (int j = tid; j < a.num_seqs; j += kThreads) {
     const int lo = a.cu_new[j], hi = a.cu_new[j + 1];
     const int p0 = a.pos0[j];
-    const int k0 = max(lo, t0), k1 = min(hi, min(t0 + kTokens, a.num_new_tokens));
+    const int k0 = max(lo, t0), k1 = min(hi, t0 + n_tok);
     for (int k = k0; k < k1; ++k) {
       s_seq[k - t0] = j;
       s_pos[k - t0] = p0 + (k - lo);
@@ -91,40 +117,30 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
   }
   __syncthreads();
 
-  // Store one pass's chunks to their slots.
-#define BROS_KVW_STORE(base, arr)                                                                   \
-  _Pragma("unroll") for (int it = 0; it < kMaxIter; ++it) {                                         \
-    const int idx = (base) + it * kThreads + tid;                                                   \
-    if (idx < total) {                                                                              \
-      BROS_KVW_SPLIT(idx)                                                                           \
-      const int h = c / kChunksPerRow;                                                              \
-      const int cc = c - h * kChunksPerRow;                                                         \
-      const int dst = s_dst[tok];                                                                   \
-      if (dst >= 0 && t0 + tok < a.num_new_tokens) {                                                \
-        const int blk = dst >> 4, slot = dst & 15;                                                  \
-        const size_t off = (((size_t)blk * a.num_kv_heads + h) * kBlockSize + slot) * row_bytes +   \
-                           (size_t)cc * 16;                                                         \
-        *reinterpret_cast<v4u_t*>((tensor ? vpool : kpool) + off) = arr[it];                        \
-      }                                                                                             \
-    }                                                                                               \
-  }
-  BROS_KVW_STORE(0, data)
+  // Store one pass's chunks to their slots: row (blk * Hkv + h) * 16 + slot.
+  auto store = [&](const Chunk& k, const v4u_t& v) {
+    if (!k.live) return;
+    const int dst = s_dst[k.tok];
+    if (dst < 0) return;
+    const size_t row0 = (size_t)(dst >> 4) * a.num_kv_heads * kBlockSize + (dst & 15);   // h = 0
+    *reinterpret_cast<v4u_t*>((k.tensor ? vpool : kpool) + row0 * kRowBytes + k.part) = v;
+  };
+#pragma unroll
+  for (int it = 0; it < kMaxIter; ++it) store(ch[it], data[it]);
   // Further passes (more KV heads than one pass holds): load, then store.
   for (int base = kThreads * kMaxIter; base < total; base += kThreads * kMaxIter) {
     v4u_t more[kMaxIter];
+    Chunk mk[kMaxIter];
 #pragma unroll
     for (int it = 0; it < kMaxIter; ++it) {
-      const int idx = base + it * kThreads + tid;
-      if (idx < total) {
-        BROS_KVW_SPLIT(idx)
-        if (t0 + tok < a.num_new_tokens)
-          more[it] = *reinterpret_cast<const v4u_t*>((tensor ? vnew : knew) + ((size_t)(t0 + tok) * chunks_per_token + c) * 16);
-      }
+      mk[it] = split(base + it * kThreads + tid);
+      if (mk[it].live)
+        more[it] = *reinterpret_cast<const v4u_t*>((mk[it].tensor ? vnew : knew) +
+                                                     ((size_t)(t0 + mk[it].tok) * chunks_per_token + mk[it].c) * 16);
     }
-    BROS_KVW_STORE(base, more)
+#pragma unroll
+    for (int it = 0; it < kMaxIter; ++it) store(mk[it], more[it]);
   }
-#undef BROS_KVW_STORE
-#undef BROS_KVW_SPLIT
 }
 
 }  // namespace
