@@ -165,16 +165,19 @@ using Int = std::integral_constant<int, N>;
 
 // Key tiles of unit (s, t): the keys its last row sees, in tiles of kKeys; 0
 // for a tile past the sequence's rows or inconsistent lengths.
-__device__ __forceinline__ int unit_tiles(const PrefillArgs& a, int s, int t, int qt) {
-  const int q_begin = a.cu_q[s];
-  const int n = a.cu_q[s + 1] - q_begin;
+// The same from the sequence's lengths: first row q_begin, n rows, context ctx_s.
+__device__ __forceinline__ int unit_tiles_of(const PrefillArgs& a, int q_begin, int n, int ctx_s, int t, int qt) {
   const int t0 = t * qt;
   if (q_begin < 0 || n <= 0 || q_begin + n > a.num_q_tokens || t0 >= n) return 0;
-  const int c0 = a.ctx_lens[s] - n;
+  const int c0 = ctx_s - n;
   if (c0 < 0) return 0;
-  const int ctx = min(a.ctx_lens[s], min(a.max_ctx, a.max_blocks_per_seq * kBlockSize));
+  const int ctx = min(ctx_s, min(a.max_ctx, a.max_blocks_per_seq * kBlockSize));
   const int kend = min(ctx, c0 + min(n, t0 + qt));
   return (kend + kKeys - 1) / kKeys;
+}
+__device__ __forceinline__ int unit_tiles(const PrefillArgs& a, int s, int t, int qt) {
+  const int q_begin = a.cu_q[s];
+  return unit_tiles_of(a, q_begin, a.cu_q[s + 1] - q_begin, a.ctx_lens[s], t, qt);
 }
 
 // Inclusive prefix sum of v over the workgroup's threads (thread order);
@@ -247,6 +250,7 @@ struct PiecePlan {
   int part;
   int parts;
   int first_slot;
+  int q_begin, n, ctx;   // the item's sequence: cu_q[s], cu_q[s + 1] - cu_q[s], ctx_lens[s] (n = -1: not read)
 };
 
 // The piece of rank `rank` (longest first). Items are (sequence, tile of
@@ -256,9 +260,10 @@ struct PiecePlan {
 // mean work of a compute unit, and an item becomes ceil(L / T) pieces; then
 // ranks exceed the items by at most num_cus / Hkv and split pieces times Hkv
 // number at most 2 num_cus. Workgroup 0 writes the list of split items for
-// the merge. `scratch` is 2 kMaxPieces + 4 + kThreads / kWave ints of LDS,
-// 16-byte aligned, that nothing else uses meanwhile. Every thread of the
-// workgroup calls it.
+// the merge. `scratch` is 2 kMaxPieces + 4 + kThreads / kWave + 3
+// kMaxRankItems ints of LDS, 16-byte aligned, that nothing else uses
+// meanwhile. Every thread of the workgroup calls it. The lengths read for the
+// ranking come back with the plan, so the unit does not read them again.
 template <int QT>
 __device__ PiecePlan plan_pieces(const PrefillArgs& a, int rank, int* scratch) {
   const int tid = threadIdx.x;
@@ -267,13 +272,30 @@ __device__ PiecePlan plan_pieces(const PrefillArgs& a, int rank, int* scratch) {
   if (n_items > kMaxRankItems) {
     // (never split) the longest tile of every sequence first
     const int t_rank = rank / a.num_seqs;
-    return PiecePlan{t_rank < tps ? (rank % a.num_seqs) * tps + (tps - 1 - t_rank) : -1, 0, 1, 0};
+    return PiecePlan{t_rank < tps ? (rank % a.num_seqs) * tps + (tps - 1 - t_rank) : -1, 0, 1, 0, 0, -1, 0};
   }
   int* s_len = scratch;                     // [kMaxPieces] lengths, then -1 padding
   int* s_pid = scratch + kMaxPieces;        // [kMaxPieces] item * 1024 + part
   int* s_res = scratch + 2 * kMaxPieces;    // [4]
   int* s_red = s_res + 4;                   // [kThreads / kWave]
-  const int L = tid < n_items ? unit_tiles(a, tid / tps, tid % tps, QT) : -1;
+  int* s_seq = s_red + kThreads / kWave;    // [3 kMaxRankItems] per item: q_begin, n, ctx
+  int L = -1;
+  if (tid < n_items) {
+    const int sq = tid / tps;
+    const int q0 = a.cu_q[sq], q1 = a.cu_q[sq + 1], cx = a.ctx_lens[sq];
+    L = unit_tiles_of(a, q0, q1 - q0, cx, tid % tps, QT);
+    s_seq[3 * tid] = q0;
+    s_seq[3 * tid + 1] = q1 - q0;
+    s_seq[3 * tid + 2] = cx;
+  }
+  auto lens_of = [&](PiecePlan p) -> PiecePlan {   // (the item's entries were written before a barrier)
+    if (p.item >= 0) {
+      p.q_begin = s_seq[3 * p.item];
+      p.n = s_seq[3 * p.item + 1];
+      p.ctx = s_seq[3 * p.item + 2];
+    }
+    return p;
+  };
   int P = 1, n_pieces = n_items, pbase = tid, sbase = 0;
   bool split = false;
   if (a.num_cus > 0) {
@@ -309,8 +331,9 @@ __device__ PiecePlan plan_pieces(const PrefillArgs& a, int rank, int* scratch) {
   if (!split) {
     if (tid < kMaxRankItems) s_len[tid] = L;   // -1 past the items
     const int k = find_rank(s_len, n_items, rank, s_res);
+    const PiecePlan out = lens_of(PiecePlan{k, 0, 1, 0, 0, -1, 0});
     __syncthreads();   // the scratch is the caller's again
-    return PiecePlan{k, 0, 1, 0};
+    return out;
   }
   if (tid < n_items) {
     for (int q = 0; q < P; ++q) {
@@ -320,7 +343,7 @@ __device__ PiecePlan plan_pieces(const PrefillArgs& a, int rank, int* scratch) {
   }
   if (tid < ((n_pieces + 3) & ~3) - n_pieces) s_len[n_pieces + tid] = -1;   // padding
   const int k = find_rank(s_len, n_pieces, rank, s_res);
-  PiecePlan out{-1, 0, 0, 0};
+  PiecePlan out{-1, 0, 0, 0, 0, -1, 0};
   if (k >= 0) {
     const int id = s_pid[k];
     const int item = id / 1024;
@@ -329,7 +352,7 @@ __device__ PiecePlan plan_pieces(const PrefillArgs& a, int rank, int* scratch) {
       s_res[2] = sbase;
     }
     __syncthreads();
-    out = PiecePlan{item, id % 1024, s_res[1], s_res[2]};
+    out = lens_of(PiecePlan{item, id % 1024, s_res[1], s_res[2], 0, -1, 0});
   }
   __syncthreads();   // the scratch is the caller's again
   return out;
@@ -392,10 +415,17 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   const int s = item / tps;
   const int t = item % tps;
 
-  // The unit's lengths, as scalar loads.
-  const int q_begin = load_uniform(a.cu_q, s);
-  const int n = load_uniform(a.cu_q, s + 1) - q_begin;
-  const int ctx_s = load_uniform(a.ctx_lens, s);
+  // The unit's lengths: from the ranking, else as scalar loads.
+  int q_begin, n, ctx_s;
+  if (__builtin_amdgcn_readfirstlane(plan.n) >= 0) {
+    q_begin = __builtin_amdgcn_readfirstlane(plan.q_begin);
+    n = __builtin_amdgcn_readfirstlane(plan.n);
+    ctx_s = __builtin_amdgcn_readfirstlane(plan.ctx);
+  } else {
+    q_begin = load_uniform(a.cu_q, s);
+    n = load_uniform(a.cu_q, s + 1) - q_begin;
+    ctx_s = load_uniform(a.ctx_lens, s);
+  }
   const int t0 = t * QT;
   if (q_begin < 0 || n <= 0 || q_begin + n > a.num_q_tokens || t0 >= n || ctx_s < n) return;
   const int c0 = ctx_s - n;
