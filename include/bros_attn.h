@@ -434,7 +434,7 @@ int bros_check_batch(const int32_t* block_tables, int32_t max_blocks_per_seq,
  * blocks with the most empty slots (a free block first); for RT requests
  * FindPreemptBlock takes BE blocks, again those with the most empty slots,
  * and writes from the opposite end; once a shared block's slots run out, only
- * the peer tokens about to be overwritten are checkpointed (lazy
+ * the peer's tokens that a write would replace are saved first (lazy
  * checkpointing), the block enters the preemption table, and the tokens come
  * back when their request is scheduled again. Sec. 4.2: Alg. 1 (priority-
  * based packing) and adaptive batch sizing.

@@ -56,3 +56,14 @@ def test_prefill_chunks_and_fp32():
                  new_counts=[130, 40, 1, 1], spare_blocks=4)
     announce("kv_write fp32 with 130- and 40-token chunks")
     check_bitwise(b, run_write(b))
+
+
+@pytest.mark.parametrize("hkv,dtype", [(1, "bf16"), (3, "bf16"), (5, "f32"), (24, "bf16"), (40, "f32")])
+def test_kv_head_counts(hkv, dtype):
+    # a token's chunks are split into (token, tensor, head, chunk) by a quotient
+    # with a runtime divisor (chunks per token); head counts that are not powers
+    # of two, and counts whose chunks take several passes of the workgroup
+    b = W.custom([37, 16, 5, 70, 2], [W.RT, W.BE, W.BE, W.RT, W.RT], hkv, hkv, dtype=dtype, seed=50 + hkv,
+                 num_prefill=1, new_counts=[21, 1, 1, 1, 1], spare_blocks=3)
+    announce(f"kv_write Hkv={hkv} {dtype}")
+    check_bitwise(b, run_write(b))
