@@ -57,10 +57,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 5000099.2, 19926.4),
-    "llama3-8b-decode": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 457538.1, 5694.7),
-    "llama3-8b-mixed-step": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 1132533.0, 7113.0),
-    "llama3-8b-pressure": ("6e70afb5e40b5a459481eab9bbf31288ce497223b563c60cf320b4e12132898b", 606221.0, 11956.6),
+    "llama3-70b-decode": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 4999790.2, 19925.9),
+    "llama3-8b-decode": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 457505.5, 5694.6),
+    "llama3-8b-mixed-step": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 1132513.8, 7112.8),
+    "llama3-8b-pressure": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 605723.6, 11957.9),
 }
 
 
