@@ -11,7 +11,7 @@ namespace dm {
 template <int G>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ int s_pre[kMaxRowsLds + 1];
-  __shared__ int s_scan[kThreads];
+  __shared__ int s_scan[kWaves];
 
   const int chunk = (a.num_rows + kMaxRowsLds - 1) / kMaxRowsLds;
   const int nch = (a.num_rows + chunk - 1) / chunk;

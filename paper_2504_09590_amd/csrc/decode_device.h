@@ -93,35 +93,59 @@ __device__ __forceinline__ int row_tiles(const DecodeArgs& a, int row) {
 // Prefix of tiles over rows in LDS: entry c is the first tile of row c * chunk
 // (chunk = 1 up to kMaxRowsLds rows). Workgroup 0 also stores the per-row
 // prefix in the workspace for the merge kernel. Returns the total tile count.
+// Each thread totals a run of consecutive chunks, parking each chunk's count
+// in its own entry; a scan within each wave and one across the waves (one
+// barrier) gives every thread its start, and the thread turns its entries
+// into prefixes. `s_scan` holds kThreads / kWave ints.
 static __device__ int build_tile_prefix(const DecodeArgs& a, int* s_pre, int* s_scan, int chunk, int nch) {
   const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), w = tid / kWave;
   const int per = (nch + kThreads - 1) / kThreads;   // chunks per thread
-  const int c0 = tid * per;
+  const int c0 = tid * per, c1 = min(nch, c0 + per);
   int mine = 0;
-  for (int c = c0; c < min(nch, c0 + per); ++c)
-    for (int r = c * chunk; r < min(a.num_rows, (c + 1) * chunk); ++r) mine += row_tiles(a, r);
-  s_scan[tid] = mine;
-  __syncthreads();
-  for (int off = 1; off < kThreads; off <<= 1) {
-    const int v = tid >= off ? s_scan[tid - off] : 0;
-    __syncthreads();
-    s_scan[tid] += v;
-    __syncthreads();
+  for (int c = c0; c < c1; ++c) {
+    int t = 0;
+    for (int r = c * chunk; r < min(a.num_rows, (c + 1) * chunk); ++r) t += row_tiles(a, r);
+    s_pre[c] = t;   // (this thread's entry: its count for now)
+    mine += t;
   }
-  int run = s_scan[tid] - mine;
-  for (int c = c0; c < min(nch, c0 + per); ++c) {
+  int inc = mine;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int u = __shfl_up(inc, o);
+    if (lane >= o) inc += u;
+  }
+  if (lane == kWave - 1) s_scan[w] = inc;
+  __syncthreads();
+  int run = inc - mine, total = 0;
+#pragma unroll
+  for (int i = 0; i < kThreads / kWave; ++i) {
+    const int x = s_scan[i];
+    run += i < w ? x : 0;
+    total += x;
+  }
+  for (int c = c0; c < c1; ++c) {
+    const int t = s_pre[c];
     s_pre[c] = run;
-    for (int r = c * chunk; r < min(a.num_rows, (c + 1) * chunk); ++r) {
-      if (blockIdx.x == 0) a.ws_rows[r] = run;
-      run += row_tiles(a, r);
+    if (blockIdx.x == 0) {
+      if (chunk == 1) {
+        a.ws_rows[c] = run;
+      } else {
+        int rr = run;
+        for (int r = c * chunk; r < min(a.num_rows, (c + 1) * chunk); ++r) {
+          a.ws_rows[r] = rr;
+          rr += row_tiles(a, r);
+        }
+      }
     }
+    run += t;
   }
   if (tid == kThreads - 1) {
-    s_pre[nch] = s_scan[kThreads - 1];
-    if (blockIdx.x == 0) a.ws_rows[a.num_rows] = s_scan[kThreads - 1];
+    s_pre[nch] = total;
+    if (blockIdx.x == 0) a.ws_rows[a.num_rows] = total;
   }
   __syncthreads();
-  return s_pre[nch];
+  return total;
 }
 
 // Where a worker stands: tile b of (row, KV head g). All fields are uniform.
