@@ -57,10 +57,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 4999790.2, 19925.9),
-    "llama3-8b-decode": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 457505.5, 5694.6),
-    "llama3-8b-mixed-step": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 1132513.8, 7112.8),
-    "llama3-8b-pressure": ("23e53d9b3adc34ba90681da57b8a674a9d7626ccdf00eb4ff7621cf90e78f255", 605723.6, 11957.9),
+    "llama3-70b-decode": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 4999658.1, 19925.6),
+    "llama3-8b-decode": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 457489.8, 5694.7),
+    "llama3-8b-mixed-step": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 1132440.6, 7113.4),
+    "llama3-8b-pressure": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 605725.6, 11957.8),
 }
 
 
