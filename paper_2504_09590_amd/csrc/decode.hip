@@ -104,44 +104,81 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void decode_mfma_merge_kernel(
   auto has_tiles = [&](int w) -> bool { return even || starts[w + 1] > starts[w]; };
   const int hl = lane / L, sub = lane % L;
   const size_t seg = (size_t)row * nkv + g;
-  // the head's max over the partials (lanes of the head take every L-th one)
-  float M = kNoMax;
-  for (int w = w0 + sub; w <= w1; w += L)
-    if (has_tiles(w)) M = fmaxf(M, a.ws_ml[2 * ((seg + w) * G + hl)]);
-#pragma unroll
-  for (int o = L / 2; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  float Lsum = 0.0f;
+  float Lsum = 0.0f, M = kNoMax;
   float acc[DPL];
 #pragma unroll
   for (int d = 0; d < DPL; ++d) acc[d] = 0.0f;
-  for (int c = w0; c <= w1; c += L) {
-    // lane sub holds the weight of partial c + sub of its head
-    float wt = 0.0f;
-    if (c + sub <= w1 && has_tiles(c + sub)) {
-      const size_t slot = (seg + c + sub) * G + hl;
-      wt = fast_exp2(a.ws_ml[2 * slot] - M);
-      Lsum = fmaf(a.ws_ml[2 * slot + 1], wt, Lsum);
-    }
-    const int cnt = min(L, w1 - c + 1);
-    for (int j0 = 0; j0 < cnt; j0 += 8) {
-      float2 v[8][DPL / 2];
-      float wj[8];
+  // Fold partials c + u, u < cnt <= 8, of the head: lane j0 + u of the head's
+  // lanes holds partial c + u's weight in wt and whether its worker had tiles
+  // (and so wrote it) in ok; v[u] holds partial c + u's dims of this lane.
+  // Padding and partials of workers without tiles add zero: their slots may
+  // hold anything.
+  auto fold8 = [&](int cnt, int j0, const float2 (&v)[8][DPL / 2], float wt, int ok) __attribute__((always_inline)) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {   // indices clamped in range; padding gets weight 0
-        const int j = min(j0 + u, cnt - 1);
-        const float w = __shfl(wt, hl * L + j);
-        wj[u] = (j0 + u < cnt) ? w : 0.0f;
-        const float2* src = reinterpret_cast<const float2*>(a.ws_acc + ((seg + c + j) * G + hl) * kHeadDim + sub * DPL);
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + min(u, cnt - 1);
+      const float w = __shfl(wt, hl * L + j);
+      const bool use = u < cnt && __shfl(ok, hl * L + j) != 0;
+      const float wu = use ? w : 0.0f;
 #pragma unroll
-        for (int q = 0; q < DPL / 2; ++q) v[u][q] = src[q];
+      for (int q = 0; q < DPL / 2; ++q) {
+        const float2 x = use ? v[u][q] : make_float2(0.0f, 0.0f);
+        acc[2 * q] = fmaf(x.x, wu, acc[2 * q]);
+        acc[2 * q + 1] = fmaf(x.y, wu, acc[2 * q + 1]);
       }
+    }
+  };
+  auto load8 = [&](int c, int cnt, float2 (&v)[8][DPL / 2]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < 8; ++u) {   // indices clamped in range
+      const int j = min(u, cnt - 1);
+      const float2* src = reinterpret_cast<const float2*>(a.ws_acc + ((seg + c + j) * G + hl) * kHeadDim + sub * DPL);
 #pragma unroll
-        for (int q = 0; q < DPL / 2; ++q) {
-          acc[2 * q] = fmaf(v[u][q].x, wj[u], acc[2 * q]);
-          acc[2 * q + 1] = fmaf(v[u][q].y, wj[u], acc[2 * q + 1]);
-        }
+      for (int q = 0; q < DPL / 2; ++q) v[u][q] = src[q];
+    }
+  };
+  if (w1 - w0 < 8) {
+    // Up to eight partials (the common case): their sums are requested
+    // together with their maxima, in one round of loads.
+    const int cnt = w1 - w0 + 1;
+    float2 v[8][DPL / 2];
+    load8(w0, cnt, v);
+    const int ok = sub < cnt && has_tiles(w0 + sub);
+    float m_l = kNoMax, l_l = 0.0f;
+    if (ok) {
+      const size_t slot = (seg + w0 + sub) * G + hl;
+      m_l = a.ws_ml[2 * slot];
+      l_l = a.ws_ml[2 * slot + 1];
+    }
+    M = fmaxf(M, m_l);
+#pragma unroll
+    for (int o = L / 2; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+    float wt = 0.0f;
+    if (ok) {
+      wt = fast_exp2(m_l - M);
+      Lsum = fmaf(l_l, wt, Lsum);
+    }
+    fold8(cnt, 0, v, wt, ok);
+  } else {
+    // the head's max over the partials (lanes of the head take every L-th one)
+    for (int w = w0 + sub; w <= w1; w += L)
+      if (has_tiles(w)) M = fmaxf(M, a.ws_ml[2 * ((seg + w) * G + hl)]);
+#pragma unroll
+    for (int o = L / 2; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+    for (int c = w0; c <= w1; c += L) {
+      // lane sub holds the weight of partial c + sub of its head
+      float wt = 0.0f;
+      const int ok = c + sub <= w1 && has_tiles(c + sub);
+      if (ok) {
+        const size_t slot = (seg + c + sub) * G + hl;
+        wt = fast_exp2(a.ws_ml[2 * slot] - M);
+        Lsum = fmaf(a.ws_ml[2 * slot + 1], wt, Lsum);
+      }
+      const int cnt = min(L, w1 - c + 1);
+      for (int j0 = 0; j0 < cnt; j0 += 8) {
+        float2 v[8][DPL / 2];
+        load8(c + j0, min(8, cnt - j0), v);
+        fold8(min(8, cnt - j0), j0, v, wt, ok);
       }
     }
   }

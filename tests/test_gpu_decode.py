@@ -26,6 +26,8 @@ def run_decode(batch, use_dir=True, repeat=1):
     code = bros.BROS_F32 if batch.dtype == "f32" else bros.BROS_BF16
     wsb = bros.bros_attn_workspace_size(0, code, batch.num_seqs - P, batch.num_q_heads, batch.head_dim, max_ctx)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda") if wsb else None
+    if ws is not None:
+        ws.fill_(255)   # NaN in every float slot: nothing may read a partial the call did not write
     outs = []
     for _ in range(repeat):
         out.fill_(float("nan"))

@@ -20,6 +20,9 @@ def _run(batch, fused):
     from paper_2504_09590_amd.step import MixedStep
     dev = bros.to_device(batch)
     step = MixedStep(batch, dev, fused=fused)
+    for ws in (step.ws_decode, step.ws_prefill):
+        if ws is not None:
+            ws.fill_(255)   # NaN in every float slot: nothing may read a partial the call did not write
     step.out_prefill.fill_(float("nan"))
     step.out_decode.fill_(float("nan"))
     pre, dec = step.run()

@@ -43,6 +43,8 @@ def run_prefill(batch, workspace=True, ws_bytes=None, stream=None):
     if ws_bytes is not None:
         wsb = ws_bytes
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda") if wsb and workspace else None
+    if ws is not None:
+        ws.fill_(255)   # NaN in every float slot: nothing may read a partial the call did not write
     bros.bros_attn_prefill_chunk(out, dev.q_prefill, dev.cu_q, max_q, dev.k_pool, dev.v_pool,
                                  dev.block_tables[:P], dev.dir[:P], dev.cls[:P], dev.ctx_lens[:P], max_ctx,
                                  workspace=ws, stream=stream)
