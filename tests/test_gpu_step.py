@@ -84,3 +84,38 @@ def test_mixed_step_replays_from_a_hip_graph(mixed):
     compare(eager[1], dec_ref, "bf16", "step decode (eager)")
     for name, ref, got in (("k", k1, dev.k_pool), ("v", v1, dev.v_pool)):
         assert np.array_equal(bros.to_host_bits(got), ref), f"{name} pool after the replays"
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_table_entries_past_the_context_are_never_used(fused):
+    """Entries at index >= ceil(ctx / 16) of a block table are not the
+    sequence's (the ABI ignores them): filled with garbage (out-of-range ids,
+    negative ids, other sequences' blocks), the step gives the same pools and
+    outputs as the oracle's step on the clean tables."""
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    from paper_2504_09590_amd.step import MixedStep
+    from tests.gpu_helpers import poison_unowned
+    ctx = [64 + 130, 45, 2000, 700, 31, 17, 400]
+    cls = [W.RT, W.RT, W.BE, W.RT, W.BE, W.BE, W.RT]
+    new = [130, 45, 1, 1, 1, 1, 1]
+    b = W.custom(ctx, cls, 32, 8, seed=71, num_prefill=2, new_counts=new, spare_blocks=6)
+    poison_unowned(b)
+    ref = oracle_step(b)
+    rng = np.random.default_rng(71)
+    garbage = np.array([2**31 - 1, -2**31, -1, -7, b.num_blocks, b.num_blocks + 5, 0, 3], dtype=np.int64)
+    nblk = (b.ctx_lens.astype(np.int64) + 15) // 16
+    for s in range(b.num_seqs):
+        tail = b.block_tables[s, nblk[s]:]
+        tail[:] = rng.choice(garbage, size=tail.shape).astype(np.int32)
+    announce(f"step with garbage past each table's context, fused={fused}")
+    dev = bros.to_device(b)
+    step = MixedStep(b, dev, fused=fused)
+    pre, dec = step.run()
+    torch.cuda.synchronize()
+    step.close()
+    k1, v1, pre_ref, dec_ref = ref
+    for name, r, got in (("k", k1, dev.k_pool), ("v", v1, dev.v_pool)):
+        assert np.array_equal(bros.to_host_bits(got), r), f"{name} pool after the step"
+    compare(bros.to_host_bits(pre), pre_ref, "bf16", "prefill with garbage table tails")
+    compare(bros.to_host_bits(dec), dec_ref, "bf16", "decode with garbage table tails")
