@@ -189,3 +189,30 @@ def test_workspace_reused_across_batches():
     compare(outs[0], ref_decode(a), "bf16", "first batch")
     compare(outs[1], ref_decode(c), "bf16", "second batch")
     assert np.array_equal(outs[0], outs[2])
+
+
+def test_calls_on_two_streams_at_once():
+    # Calls on different streams with workspaces of their own may run at the
+    # same time: the library keeps no state between calls but per-device
+    # queries, so each gives what it gives alone.
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    a = W.custom([9000, 40, 3000, 17, 700], [W.BE, W.RT, W.BE, W.RT, W.BE], 32, 8, seed=15)
+    c = W.custom([5000, 2000, 33, 12000], [W.BE, W.BE, W.RT, W.BE], 32, 8, seed=16)
+    devs, outs, wss = [], [], []
+    for x in (a, c):
+        dev = bros.to_device(x)
+        devs.append(dev)
+        outs.append(torch.full_like(dev.q_decode, float("nan")))
+        wsb = bros.bros_attn_workspace_size(0, bros.BROS_BF16, x.num_seqs, 32, 128, int(x.ctx_lens.max()))
+        wss.append(torch.full((wsb,), 255, dtype=torch.uint8, device="cuda"))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    announce("decode on two streams at once")
+    for _ in range(3):
+        for x, dev, out, ws, st in zip((a, c), devs, outs, wss, streams):
+            bros.bros_attn_decode(out, dev.q_decode, dev.k_pool, dev.v_pool, dev.block_tables, dev.dir, dev.cls,
+                                  dev.ctx_lens, int(x.ctx_lens.max()), workspace=ws, stream=st)
+    torch.cuda.synchronize()
+    compare(bros.to_host_bits(outs[0]), ref_decode(a), "bf16", "stream 1")
+    compare(bros.to_host_bits(outs[1]), ref_decode(c), "bf16", "stream 2")
