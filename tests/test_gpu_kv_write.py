@@ -67,3 +67,19 @@ def test_kv_head_counts(hkv, dtype):
                  num_prefill=1, new_counts=[21, 1, 1, 1, 1], spare_blocks=3)
     announce(f"kv_write Hkv={hkv} {dtype}")
     check_bitwise(b, run_write(b))
+
+
+def test_direction_from_class_when_flags_are_null():
+    # dir = NULL: each sequence's direction comes from its class (RT from the
+    # left end, BE from the right end), as the flags would give it
+    torch = require_gpu()
+    from paper_2504_09590_amd import bros
+    b = W.custom([16 + 6, 16 * 3 + 10, 5, 11, 70], [W.RT, W.BE, W.RT, W.BE, W.BE], 8, 8, seed=42,
+                 num_prefill=1, new_counts=[22, 1, 1, 1, 1])
+    assert np.array_equal(b.dir, np.where(b.cls == W.RT, 1, -1).astype(np.int8))
+    dev = bros.to_device(b)
+    announce("kv_write with null direction flags")
+    bros.bros_kv_write(dev.k_new, dev.v_new, dev.k_pool, dev.v_pool, dev.block_tables, None, dev.cls,
+                       dev.pos0, dev.cu_new)
+    torch.cuda.synchronize()
+    check_bitwise(b, dev)
