@@ -62,10 +62,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 4999658.1, 19925.6),
-    "llama3-8b-decode": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 457489.8, 5694.7),
-    "llama3-8b-mixed-step": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 1132440.6, 7113.4),
-    "llama3-8b-pressure": ("a6121f1c19e516096fbcdc11937600abaad6878304f894d07d5aea522a966ae8", 605725.6, 11957.8),
+    "llama3-70b-decode": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 4999735.7, 19926.1),
+    "llama3-8b-decode": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 457517.7, 5694.5),
+    "llama3-8b-mixed-step": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 1132459.6, 7113.4),
+    "llama3-8b-pressure": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 605743.3, 11958.0),
 }
 
 
