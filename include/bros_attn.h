@@ -112,7 +112,8 @@ int bros_abi_version(void);
  *   cu_new       : int32 [num_seqs + 1], prefix offsets of new tokens; cu_new[0] = 0,
  *                  cu_new[num_seqs] = num_new_tokens
  * num_new_tokens == 0 is a no-op. A token whose block-table entry is out of
- * range (see COMMON CONVENTIONS) is skipped.
+ * range (see COMMON CONVENTIONS) is skipped. num_kv_heads above 16384 is
+ * BROS_E_UNSUPPORTED.
  */
 int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
                   void* k_pool, void* v_pool, int32_t num_blocks,

@@ -72,6 +72,8 @@ int bros_kv_write(const void* k_new, const void* v_new, int32_t num_new_tokens,
   int st = check_shapes(fn, num_kv_heads, num_kv_heads, head_dim, block_size, dtype, &group);
   if (st) return st;
   if (num_new_tokens < 0 || num_seqs < 0) return fail(BROS_E_SHAPE, "%s: negative count (tokens=%d seqs=%d)", fn, num_new_tokens, num_seqs);
+  // (a workgroup's chunk indices stay below 2^22, where the kernel's float quotient is exact)
+  if (num_kv_heads > 16384) return fail(BROS_E_UNSUPPORTED, "%s: %d KV heads; at most 16384", fn, num_kv_heads);
   if (num_new_tokens == 0) return ok();
   if (num_seqs == 0) return fail(BROS_E_SHAPE, "%s: %d new tokens but no sequences", fn, num_new_tokens);
   if (!k_new || !v_new || !k_pool || !v_pool || !pos0 || !cu_new) return fail(BROS_E_NULL, "%s: a tensor or offset pointer is NULL", fn);

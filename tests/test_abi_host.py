@@ -98,6 +98,8 @@ def test_kv_write_rejects():
     assert L.bros_kv_write(*a) == -2         # direction mode
     a = list(args); a[2] = 0
     assert L.bros_kv_write(*a) == 0          # no tokens: no-op
+    a = list(args); a[14] = 16385
+    assert L.bros_kv_write(*a) == -4         # more KV heads than the kernel's index split covers
 
 
 def test_prefill_rejects():
