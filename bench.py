@@ -11,8 +11,9 @@ U{512..8192}, 32 q / 8 KV heads, head_dim 128, bf16, 40000-block pool).
 Timing: inputs resident in HBM; W untimed warm-up steps, then timed passes of
 exactly K steps each, every pass between two synchronizations: one that
 brackets every call with HIP events (the per-call figures), one with HIP
-events around the decode call on the stream it runs on (the roofline's launch
-duration), the headline pass, with HIP events only around the K steps (an
+events around the decode call on the stream it runs on and, recorded by the
+library, around the decode kernel inside it (the roofline's launch duration),
+the headline pass, with HIP events only around the K steps (an
 event inside a step costs it a few microseconds), and the per-call pass again.
 The GPU's clocks ramp up over the first ~30 steps after it has been idle
 (10-step batches right after start: 440, 424, 418, then 416 us), so the
@@ -22,8 +23,11 @@ first one's are in per_call_us_first_pass). Then R single steps, each
 after a scrub that reads and writes 1 GiB outside its events, give the median,
 p10 and p90 of a step whose KV comes from HBM. Prints ONE JSON line:
   value     = algorithmic bytes of a step / step time (GB/s, whole job)
-  roofline  = the dominant call (decode): algorithmic bytes per launch / its
-              average event-timed duration, against 8 TB/s HBM
+  roofline  = the dominant kernel (the decode kernel): the decode's algorithmic
+              bytes per launch / that kernel's average duration between HIP
+              events the library records around it on its stream, against 8
+              TB/s HBM; call_frac is the same over the whole decode call
+              (kernel and merge, events around the call in the per-call pass)
   scrubbed  = p10 / p50 / p90 of the scrubbed single steps
   cpu_baseline = the CPU oracle timed on one host core over one whole step
               (or, when the pools do not fit in float64, a sample of rows).
@@ -50,8 +54,8 @@ FP64_POOL_LIMIT = 16e9
 # Bytes the scrub between timed repetitions reads and writes (4x the 256 MiB last-level cache).
 SCRUB_BYTES = 1 << 30
 
-# HBM traffic of the decode call from rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, one
-# counter per run, KiB per dispatch, summed over decode_mfma_kernel and decode_mfma_merge_kernel).
+# HBM traffic of the decode kernel from rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, one
+# counter per run, KiB per dispatch of decode_mfma_kernel).
 # The counters are scaled by what they read for a plain 1 GiB device copy
 # (--calibrate-copy): FETCH_SIZE reads half the bytes copied, WRITE_SIZE all of them.
 FETCH_SCALE = 2.0
@@ -284,10 +288,25 @@ def main():
         prefilled = [torch.cuda.Event() for _ in range(K)]
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
+        # the decode kernel alone, apart from its merge: events the library
+        # records around that kernel inside the bracketed decode call
+        kev = None
+        if bracket == "main" and main_call == "decode" and batch.dtype == "bf16":
+            kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+            for a, b in kev:   # (a torch event exists once it has been recorded)
+                a.record(stream); b.record(stream)
+
         def call(name, i, s, fn):
             if name in ev:
                 a, b = ev[name][i]
-                a.record(s); fn(s); b.record(s)
+                a.record(s)
+                if kev is not None and name == "decode":
+                    bros.bros_set_decode_kernel_events(*kev[i])
+                    fn(s)
+                    bros.bros_set_decode_kernel_events(None, None)
+                else:
+                    fn(s)
+                b.record(s)
             else:
                 fn(s)
 
@@ -320,6 +339,8 @@ def main():
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t0) * 1e3
         per = {k: float(np.mean([a.elapsed_time(b) for a, b in pairs])) for k, pairs in ev.items()}
+        if kev is not None:
+            per["decode_kernel"] = float(np.mean([a.elapsed_time(b) for a, b in kev]))
         return start.elapsed_time(end) / K, per, wall
 
     def scrubbed_reps(R: int):
@@ -368,23 +389,34 @@ def main():
     ms_main, per_main, _ = timed_steps("main")
     ms, _, wall_ms = timed_steps("none")
     ms_inst, per_call, _ = timed_steps("all")
-    per_call[main_call + "_alone_bracketed"] = per_main[main_call]
+    if "decode_kernel" in per_main:
+        per_call["decode_kernel"] = per_main["decode_kernel"]   # the roofline pass: the kernel alone
+    else:
+        per_call[main_call + "_alone_bracketed"] = per_main[main_call]
     reps = scrubbed_reps(max(args.reps, 1))
 
-    dec_ms = per_main.get(main_call)
+    call_ms = per_main.get(main_call)
+    # the whole call as the per-call pass times it (no event between its kernels)
+    call_alone_ms = per_call.get(main_call, call_ms)
     roof = None
-    if dec_ms:
+    if call_ms:
         if step.fused:
             nbytes = work["decode"]["bytes"] + work["prefill"]["bytes"]
-            kernel, traffic = "bros_attn_mixed (mixed_kernel + decode_mfma_merge_kernel)", None
+            kernel, traffic, dec_ms = "bros_attn_mixed (mixed_kernel + decode_mfma_merge_kernel)", None, call_ms
+        elif "decode_kernel" in per_main:
+            # the dominant kernel on its own; the whole call (kernel + merge) beside it
+            nbytes = work["decode"]["bytes"]
+            kernel, dec_ms = "decode_mfma_kernel", per_main["decode_kernel"]
+            traffic = decode_traffic(batch.name)
         else:
             nbytes = work["decode"]["bytes"]
-            kernel = "bros_attn_decode (decode_mfma_kernel + decode_mfma_merge_kernel)"
-            traffic = decode_traffic(batch.name)
+            kernel, traffic, dec_ms = "bros_attn_decode (decode kernel + merge)", None, call_ms
         achieved = nbytes / (dec_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kernel,
-                "bytes_per_launch": nbytes, "avg_launch_us": round(dec_ms * 1e3, 2)}
+                "bytes_per_launch": nbytes, "avg_launch_us": round(dec_ms * 1e3, 2),
+                "call_avg_us": round(call_alone_ms * 1e3, 2),
+                "call_frac": round(nbytes / (call_alone_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
 
     value = work["step_bytes"] / (ms * 1e-3) / 1e9
     line = {

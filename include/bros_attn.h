@@ -382,6 +382,23 @@ int bros_slot_ids(const int32_t* block_tables, int32_t max_blocks_per_seq, const
                   const int32_t* seqs, const int32_t* positions, int32_t n, int32_t* slot_ids);
 
 /*
+ * bros_set_decode_kernel_events -- measurement hook for benchmarks.
+ *
+ * Not an operation of the paper: it lets a benchmark time the decode kernel
+ * on its own, apart from the merge kernel that ends every bf16
+ * bros_attn_decode call. With both events non-NULL (hipEvent_t handles, owned
+ * by the caller, created with timing enabled), every following bf16
+ * bros_attn_decode or bros_attn_decode_noalloc call records `before` on its
+ * stream right before its decode kernel and `after` right after it, ahead of
+ * the merge; hipEventElapsedTime(before, after) is then that kernel's
+ * duration. NULL, NULL (the default) records nothing. The setting is
+ * process-wide: set it from one thread, with no decode call in flight on
+ * another. A failed record is reported by the decode call as BROS_E_HIP.
+ * Returns BROS_OK, or BROS_E_NULL when exactly one event is NULL.
+ */
+int bros_set_decode_kernel_events(void* before, void* after);
+
+/*
  * bros_stream_create_cu_share -- a stream whose kernels run on a fixed share
  * of the current device's compute units.
  *

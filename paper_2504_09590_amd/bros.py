@@ -30,7 +30,7 @@ EXPORTED = ["bros_status_str", "bros_last_error", "bros_abi_version", "bros_kv_w
             "bros_mgr_create", "bros_mgr_destroy", "bros_mgr_add_request", "bros_mgr_release", "bros_mgr_grow",
             "bros_mgr_restore", "bros_mgr_query", "bros_mgr_table", "bros_mgr_free_blocks", "bros_mgr_validate", "bros_mgr_available",
             "bros_mgr_entries_needed", "bros_mgr_preemption_table", "bros_schedule", "bros_next_batch_size",
-            "bros_mgr_grow_batch", "bros_mgr_plan_bound", "bros_schedule_pulled"]
+            "bros_mgr_grow_batch", "bros_mgr_plan_bound", "bros_schedule_pulled", "bros_set_decode_kernel_events"]
 
 
 class BrosError(RuntimeError):
@@ -64,6 +64,8 @@ def _load() -> ctypes.CDLL:
     lib.bros_attn_prefill_chunk.restype = ctypes.c_int
     lib.bros_attn_mixed.argtypes = [P, P, P, I, I, I, I, P, P, I, I, P, P, I, P, I, P, P, I, P, I, I, I, I, F, I, P, Z, P]
     lib.bros_attn_mixed.restype = ctypes.c_int
+    lib.bros_set_decode_kernel_events.argtypes = [P, P]
+    lib.bros_set_decode_kernel_events.restype = ctypes.c_int
     lib.bros_attn_workspace_size.argtypes = [I, I, I, I, I, I]
     lib.bros_attn_workspace_size.restype = Z
     lib.bros_check_batch.argtypes = [P, I, P, P, I, P, I, I, I, I]
@@ -145,6 +147,14 @@ def bros_kv_write(k_new, v_new, k_pool, v_pool, block_tables, dir, cls, pos0, cu
                              _ptr(block_tables), int(block_tables.shape[1]), _ptr(dir), _ptr(cls),
                              _dir_mode(dir, block_tables), _ptr(pos0), _ptr(cu_new), int(cu_new.shape[0]) - 1, hkv, d, bs,
                              _dtype_code(k_pool), _stream(stream)))
+
+
+def bros_set_decode_kernel_events(before=None, after=None):
+    """Measurement hook: later bf16 decode calls record these torch.cuda.Events
+    (timing enabled, each recorded once already so that it exists) right
+    before and right after their decode kernel; None, None turns it off."""
+    handle = (lambda e: None if e is None else ctypes.c_void_p(e.cuda_event))
+    _check(LIB.bros_set_decode_kernel_events(handle(before), handle(after)))
 
 
 def bros_attn_workspace_size(kind: int, dtype: int, num_rows: int, num_q_heads: int,

@@ -395,6 +395,13 @@ int bros_kv_scatter(const void* k_in, const void* v_in,
                  const_cast<void*>(k_in), const_cast<void*>(v_in), num_kv_heads, head_dim, block_size, dtype, stream);
 }
 
+int bros_set_decode_kernel_events(void* before, void* after) {
+  if ((before == nullptr) != (after == nullptr))
+    return fail(BROS_E_NULL, "bros_set_decode_kernel_events: give both events or neither");
+  bros::set_decode_kernel_events(static_cast<hipEvent_t>(before), static_cast<hipEvent_t>(after));
+  return ok();
+}
+
 int bros_stream_create_cu_share(int32_t first_cu, int32_t num_cus, void** stream) {
   const char* fn = "bros_stream_create_cu_share";
   if (stream == nullptr) return fail(BROS_E_NULL, "%s: stream is NULL", fn);

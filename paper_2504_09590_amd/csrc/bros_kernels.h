@@ -123,6 +123,8 @@ void set_decode_workspace(DecodeArgs& a, void* ws, bool bf16);
 hipError_t launch_kv_write(const KvWriteArgs& a, bool bf16, hipStream_t stream);
 hipError_t launch_kv_move(const KvMoveArgs& a, bool gather, hipStream_t stream);
 hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream);
+// Events the bf16 decode records around its decode kernel (both null: none).
+void set_decode_kernel_events(hipEvent_t before, hipEvent_t after);
 // Longest context the matrix-core prefill handles (its block table is staged
 // whole in LDS); longer contexts take the vector path.
 constexpr int32_t kPrefillMaxCtxMfma = 32768;

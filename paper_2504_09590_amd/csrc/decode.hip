@@ -2,6 +2,7 @@
 // segments. The device code (and what it computes) is in decode_device.h.
 #include "decode_device.h"
 
+#include <atomic>
 #include <mutex>
 #include <type_traits>
 
@@ -257,14 +258,22 @@ namespace {
 // workspace is sized for it.
 constexpr int kMaxDecodeGrid = 1024;
 
+// Events recorded around the decode kernel of every bf16 call (a
+// benchmark's hook; both null when unused).
+std::atomic<hipEvent_t> g_kernel_ev_before{nullptr}, g_kernel_ev_after{nullptr};
+
 template <int G>
 hipError_t launch_group(DecodeArgs a, hipStream_t stream, int slot) {
   int grid = resident_workgroups(reinterpret_cast<const void*>(&dm::decode_mfma_kernel<G>), kThreads, slot, stream);
   grid = grid < kMaxDecodeGrid ? grid : kMaxDecodeGrid;
   a.num_workers = grid * kWaves;
+  const hipEvent_t before = g_kernel_ev_before.load(), after = g_kernel_ev_after.load();
+  hipError_t e = hipSuccess;
+  if (before != nullptr && (e = hipEventRecord(before, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL((dm::decode_mfma_kernel<G>), dim3(grid), dim3(kThreads), 0, stream, a);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (after != nullptr && (e = hipEventRecord(after, stream)) != hipSuccess) return e;
   return launch_decode_merge(a, G, stream);
 }
 
@@ -328,6 +337,11 @@ void set_decode_workspace(DecodeArgs& a, void* ws, bool bf16) {
   a.ws_wstart = nullptr;
   a.ws_acc = reinterpret_cast<float*>(base);
   a.ws_ml = base ? a.ws_acc + (size_t)a.num_rows * a.num_q_heads * a.n_split_max * kHeadDim : nullptr;
+}
+
+void set_decode_kernel_events(hipEvent_t before, hipEvent_t after) {
+  g_kernel_ev_before.store(before);
+  g_kernel_ev_after.store(after);
 }
 
 hipError_t launch_decode(DecodeArgs a, int group, bool bf16, hipStream_t stream) {

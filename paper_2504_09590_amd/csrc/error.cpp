@@ -48,6 +48,6 @@ const char* bros_status_str(int status) {
 
 const char* bros_last_error(void) { return g_last_error.c_str(); }
 
-int bros_abi_version(void) { return 8; }
+int bros_abi_version(void) { return 9; }
 
 }  // extern "C"

@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings_and_version():
     for code, name in bros.STATUS.items():
         assert bros.LIB.bros_status_str(code).decode() == name
-    assert bros.LIB.bros_abi_version() == 8
+    assert bros.LIB.bros_abi_version() == 9
 
 
 # --- argument validation (returns before any HIP call) -----------------------
@@ -313,3 +313,10 @@ def test_slot_ids_follow_the_oracle_mapping():
         bros.bros_slot_ids(b.block_tables, b.dir, b.cls, b.num_blocks, [b.num_seqs], [0])
     with pytest.raises(bros.BrosError, match="beyond"):
         bros.bros_slot_ids(b.block_tables, b.dir, b.cls, b.num_blocks, [0], [16 * b.block_tables.shape[1]])
+
+
+def test_decode_kernel_events_hook_takes_both_or_neither():
+    L = bros.LIB
+    assert L.bros_set_decode_kernel_events(FAKE, None) == -1
+    assert L.bros_set_decode_kernel_events(None, FAKE) == -1
+    assert L.bros_set_decode_kernel_events(None, None) == 0
