@@ -66,10 +66,10 @@ DECODE_SOURCES = ("paper_2504_09590_amd/csrc/decode.hip", "paper_2504_09590_amd/
                   "paper_2504_09590_amd/csrc/bros_kernels.h")
 DECODE_COUNTERS = {
     # workload: (sha256 of DECODE_SOURCES when the counters were read, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "llama3-70b-decode": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 4999735.7, 19926.1),
-    "llama3-8b-decode": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 457517.7, 5694.5),
-    "llama3-8b-mixed-step": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 1132459.6, 7113.4),
-    "llama3-8b-pressure": ("42e57248080e9465070f24b5594889b56c090b645e044006ba94dd134cd0940a", 605743.3, 11958.0),
+    "llama3-70b-decode": ("f12efb5159ca9ddbc4bd03e7871364d4a41b058062ac265b93f1a6bc2576ee52", 4991849.4, 16514.1),
+    "llama3-8b-decode": ("f12efb5159ca9ddbc4bd03e7871364d4a41b058062ac265b93f1a6bc2576ee52", 454831.8, 5197.5),
+    "llama3-8b-mixed-step": ("f12efb5159ca9ddbc4bd03e7871364d4a41b058062ac265b93f1a6bc2576ee52", 1129273.9, 6173.5),
+    "llama3-8b-pressure": ("f12efb5159ca9ddbc4bd03e7871364d4a41b058062ac265b93f1a6bc2576ee52", 601668.8, 10115.7),
 }
 
 
