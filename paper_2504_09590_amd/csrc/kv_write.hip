@@ -4,10 +4,10 @@
 // sequence's table holds its positions [16 i, 16 i + 16)). The direction is
 // the sequence's, or that of the token's table entry (Sec. 6's table).
 //
-// One workgroup moves kTokens tokens. Its 256 threads first request the
-// tokens' source rows (16-byte chunks), which do not depend on the
-// destination; meanwhile each thread checks one sequence's range of new
-// tokens, and then one thread per token resolves its destination (position,
+// One workgroup moves kTokens tokens. Its 256 threads first request their
+// sequence ranges and the tokens' source rows (16-byte chunks), which do not
+// depend on the destination; each thread then checks one sequence's range of
+// new tokens, and one thread per token resolves its destination (position,
 // table entry, slot); then the chunks are stored. Writes are
 // slot-granular, so two sequences sharing a block never race.
 #include "bros_device.h"
@@ -79,6 +79,15 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
     return k;
   };
 
+  // This thread's first sequence range (thread j: sequence j), requested
+  // before the source rows: loads return in order, so the range check below
+  // then waits for these alone, not for the rows coming from HBM.
+  int m_lo = 0, m_hi = 0, m_p0 = 0;
+  if (tid < a.num_seqs) {
+    m_lo = a.cu_new[tid];
+    m_hi = a.cu_new[tid + 1];
+    m_p0 = a.pos0[tid];
+  }
   // Source rows of the first pass: they do not depend on where the tokens go,
   // so they are requested before the destinations are resolved.
   v4u_t data[kMaxIter];
@@ -100,8 +109,9 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(KvWriteArgs a) {
   if (tid < kTokens) s_seq[tid] = -1;
   __syncthreads();
   for (int j = tid; j < a.num_seqs; j += kThreads) {
-    const int lo = a.cu_new[j], hi = a.cu_new[j + 1];
-    const int p0 = a.pos0[j];
+    const bool first = j == tid;
+    const int lo = first ? m_lo : a.cu_new[j], hi = first ? m_hi : a.cu_new[j + 1];
+    const int p0 = first ? m_p0 : a.pos0[j];
     const int k0 = max(lo, t0), k1 = min(hi, t0 + n_tok);
     for (int k = k0; k < k1; ++k) {
       s_seq[k - t0] = j;
