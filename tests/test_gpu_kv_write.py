@@ -51,6 +51,24 @@ def test_shared_tails_written_in_one_launch():
     check_bitwise(b, run_write(b))
 
 
+@pytest.mark.parametrize("num_seqs,num_prefill", [(600, 0), (300, 3)])
+def test_more_sequences_than_threads(num_seqs, num_prefill):
+    # a workgroup's 256 threads each check one sequence's range per pass:
+    # sequences 256 and up are found on the later passes
+    rng = np.random.default_rng(43 + num_seqs)
+    ctx = [int(x) for x in rng.integers(1, 90, num_seqs)]
+    cls = [W.RT if i % 3 == 0 else W.BE for i in range(num_seqs)]
+    new_counts = None
+    if num_prefill:
+        new_counts = [1] * num_seqs
+        for s in range(num_prefill):
+            ctx[s] = 40 + 37 * s
+            new_counts[s] = 20 + 7 * s
+    b = W.custom(ctx, cls, 8, 8, seed=44 + num_seqs, num_prefill=num_prefill, new_counts=new_counts)
+    announce(f"kv_write {num_seqs} sequences, {num_prefill} chunks, tokens={int(b.cu_new[-1])}")
+    check_bitwise(b, run_write(b))
+
+
 def test_prefill_chunks_and_fp32():
     b = W.custom([300, 40, 7, 90], [W.RT, W.RT, W.BE, W.BE], 8, 2, dtype="f32", seed=41, num_prefill=2,
                  new_counts=[130, 40, 1, 1], spare_blocks=4)
