@@ -439,8 +439,6 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   const int nblk = (ctx + kBlockSize - 1) / kBlockSize;
   // keys below this logical position are visible to every row of the unit
   const int full_below = min(ctx, c0 + t0 + 1);
-  const int n_steps = n_kt;   // one tile per step
-  const int n_mine = n_kt;
 
   const int half = lane >> 5;
   const int mrow = lane & 31;
@@ -564,8 +562,8 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   floatx16 sa, sb;
   const float sl2 = a.scale_log2;
 
-  // K operands of the tile in K ring `sk` (this wave's half), all eight
-  // d-steps, issued together.
+  // K operands of the tile in K ring `sk`, all eight d-steps, issued
+  // together.
   auto k_operands = [&](const uint8_t* sk, v4u_t (&kv)[8]) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < 8; ++c) kv[c] = *reinterpret_cast<const v4u_t*>(sk + k_lane + (((2 * c) ^ (k_sw & 14)) << 4));
@@ -676,11 +674,6 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   // After step ii: wait for batch ii + 1 (K of step ii + 2, V of step ii + 1),
   // zero V's non-context rows (FIX; a tile below plain_tiles has none),
   // publish, then issue batch ii + 4 into the slots step ii freed (K slot
-  // (ii + 1) % 4, V slot ii % 4). eF, eV, eK are this wave's table entries
-  // for steps ii + 1, ii + 4 and ii + 5.
-  // After step ii: wait for batch ii + 1 (K of step ii + 2, V of step ii + 1),
-  // zero V's non-context rows (FIX; a tile below plain_tiles has none),
-  // publish, then issue batch ii + 4 into the slots step ii freed (K slot
   // (ii + 1) % 4, V slot ii % 4): K of step ii + 5 from row index ik, V of
   // step ii + 4 from iv.
   auto advance = [&](int ii, int sl, int ik, int iv, auto fixc) __attribute__((always_inline)) {
@@ -734,7 +727,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   fixup_v(0, s_vring);
   lds_barrier();
-  if (n_mine > 0) {
+  {
     v4u_t kv[8];
     k_operands(kr, kv);
     scores(kv, sa);
@@ -760,7 +753,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   int ii = 0;
   int iv = w3;
   // the piece's tiles below plain_tiles, as a step bound
-  const int n_plain = max(0, min(n_mine, plain_tiles - kb));
+  const int n_plain = max(0, min(n_kt, plain_tiles - kb));
   auto main_step = [&](auto uc) __attribute__((always_inline)) -> bool {
     constexpr int u = decltype(uc)::value;
     if (ii + 1 >= n_plain) return false;
@@ -780,7 +773,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
   }
   if (ii & 1) sa = sb;   // the rest carries the scores in `sa`
   // Tiles with a next tile that needs (or may need) the mask.
-  for (; ii + 1 < n_mine; ++ii) {
+  for (; ii + 1 < n_kt; ++ii) {
     const int sl = ii & (kSlots - 1);
     const int sl1 = (sl + 1) & (kSlots - 1);
     const int ik = own(ii + 5);
@@ -790,8 +783,8 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
     advance(ii, sl, ik, iv, std::true_type{});
     iv = ik;
   }
-  // The last tile of this wave's half.
-  if (ii < n_mine) {
+  // The last tile (no next tile to score).
+  if (ii < n_kt) {
     const int sl = ii & (kSlots - 1);
     const int ik = own(ii + 5);
     step(kr, vr + sl * kSlotBytes, 0, std::false_type{}, std::false_type{}, sa, sb);
@@ -799,13 +792,6 @@ __device__ __forceinline__ void prefill_unit(const PrefillArgs& a, int id, uint8
     iv = ik;
     ++ii;
   }
-  // Steps where only the other half has a tile.
-  for (; ii < n_steps; ++ii) {
-    const int ik = own(ii + 5);
-    advance(ii, ii & (kSlots - 1), ik, iv, std::true_type{});
-    iv = ik;
-  }
-
   wait_vmem<0>();
   const float l_run = lacc[0];
   if (parts > 1) {
